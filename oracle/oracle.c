@@ -1,0 +1,285 @@
+/*
+ * ChebBooster online stage: slow, plain fp64 CPU oracle.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing on the product path may link, load or
+ * call this file; only the test suite, the smoke check and the CPU baseline
+ * leg of the benchmark do.  It shares no code, header, table or helper with
+ * the HIP library.
+ *
+ * What it computes (paper, Section 3.2 "Chebyshev-Inspired Extrapolation",
+ * Section 3.3 "ChebBooster", Appendix A):
+ *
+ *   - barycentric weights rho_j = 1 / omega'(x_j) for arbitrary distinct
+ *     nodes (Appendix A, general-weights equation),
+ *   - interpolation coefficients w_j(x) = (rho_j / (x - x_j)) /
+ *     sum_i rho_i / (x - x_i)  (Section 3.2, coefficient equation; Appendix A,
+ *     second barycentric form), with nodes and target first mapped affinely
+ *     onto [-1, 1] (Section 3.3, weight precomputation),
+ *   - the skipped-step prediction f_t = sum_j w_j f_{s_j} (Section 3.3,
+ *     forward application equation; Algorithm 1, online stage), evaluated
+ *     per element in fp64 with the terms added oldest to newest.
+ *
+ * Floating-point storage formats are decoded exactly from their IEEE-754
+ * definitions.  All accumulation is fp64.  No blocking, no reordering, no
+ * fused shortcuts: one element at a time, one history entry at a time.
+ *
+ * Every function has pins in the CPU test suite against closed forms,
+ * exact rational Lagrange weights and the paper's equispaced-node formula.
+ */
+#include "oracle.h"
+
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+/* ------------------------------------------------------------------------ */
+/* Threads (the per-element loop is independent across elements).            */
+/* ------------------------------------------------------------------------ */
+
+int oracle_set_threads(int n) {
+#ifdef _OPENMP
+  if (n > 0) omp_set_num_threads(n);
+  return omp_get_max_threads();
+#else
+  (void)n;
+  return 1;
+#endif
+}
+
+int oracle_max_threads(void) {
+#ifdef _OPENMP
+  return omp_get_max_threads();
+#else
+  return 1;
+#endif
+}
+
+/* ------------------------------------------------------------------------ */
+/* Node checks and normalisation (Section 3.3: timesteps mapped to [-1,1]).   */
+/* ------------------------------------------------------------------------ */
+
+/* Returns 0 when every node is finite and no two are equal, else a negative
+ * code: -1 bad count, -2 non-finite node, -3 repeated node. */
+int oracle_check_nodes(const double *x, int n) {
+  if (n < 1) return -1;
+  for (int j = 0; j < n; ++j)
+    if (!isfinite(x[j])) return -2;
+  for (int j = 0; j < n; ++j)
+    for (int k = j + 1; k < n; ++k)
+      if (x[j] == x[k]) return -3;
+  return 0;
+}
+
+/* Affine map of the node span [min x, max x] onto [-1, 1]; the target goes
+ * through the same map, so |y*| > 1 means extrapolation.  With a single node
+ * there is no span and everything maps to 0. */
+void oracle_normalise(const double *x, int n, double xstar, double *y,
+                      double *ystar) {
+  double a = x[0], b = x[0];
+  for (int j = 1; j < n; ++j) {
+    if (x[j] < a) a = x[j];
+    if (x[j] > b) b = x[j];
+  }
+  if (n == 1 || b == a) {
+    for (int j = 0; j < n; ++j) y[j] = 0.0;
+    *ystar = 0.0;
+    return;
+  }
+  for (int j = 0; j < n; ++j) y[j] = (2.0 * x[j] - (a + b)) / (b - a);
+  *ystar = (2.0 * xstar - (a + b)) / (b - a);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Barycentric weights (Appendix A).                                          */
+/* ------------------------------------------------------------------------ */
+
+/* rho_j = 1 / omega'(y_j), omega'(y_j) = prod_{k != j} (y_j - y_k). */
+void oracle_barycentric_rho(const double *y, int n, double *rho) {
+  for (int j = 0; j < n; ++j) {
+    double d = 1.0;
+    for (int k = 0; k < n; ++k)
+      if (k != j) d *= (y[j] - y[k]);
+    rho[j] = 1.0 / d;
+  }
+}
+
+/* One row of interpolation coefficients for one target.  Returns 0 or the
+ * negative code of oracle_check_nodes.  A target equal to a node gets the
+ * unit vector of that node (the second form is 0/0 there, its limit is the
+ * node value). */
+int oracle_weights_row(const double *x, int n, double xstar, double *w) {
+  int rc = oracle_check_nodes(x, n);
+  if (rc) return rc;
+  if (!isfinite(xstar)) return -2;
+  for (int j = 0; j < n; ++j) {
+    if (xstar == x[j]) {
+      for (int k = 0; k < n; ++k) w[k] = (k == j) ? 1.0 : 0.0;
+      return 0;
+    }
+  }
+  double y[ORACLE_MAX_NODES], rho[ORACLE_MAX_NODES], q[ORACLE_MAX_NODES];
+  if (n > ORACLE_MAX_NODES) return -1;
+  double ystar;
+  oracle_normalise(x, n, xstar, y, &ystar);
+  if (n == 1) { /* degree-0 interpolant: the single cached value */
+    w[0] = 1.0;
+    return 0;
+  }
+  oracle_barycentric_rho(y, n, rho);
+  double denom = 0.0;
+  for (int j = 0; j < n; ++j) {
+    double diff = ystar - y[j];
+    if (diff == 0.0) { /* distinct x collapsed by the map: take the limit */
+      for (int k = 0; k < n; ++k) w[k] = (k == j) ? 1.0 : 0.0;
+      return 0;
+    }
+    q[j] = rho[j] / diff;
+    denom += q[j];
+  }
+  for (int j = 0; j < n; ++j) w[j] = q[j] / denom;
+  return 0;
+}
+
+/* Table of rows: w[m * n + j] for target m, node j (oldest to newest). */
+int oracle_weights(const double *x, int n, const double *xstar, int m,
+                   double *w) {
+  for (int i = 0; i < m; ++i) {
+    int rc = oracle_weights_row(x, n, xstar[i], w + (size_t)i * n);
+    if (rc) return rc;
+  }
+  return 0;
+}
+
+/* Lagrange product form l_j(x) = prod_{k != j} (x - x_k) / (x_j - x_k)
+ * (Appendix A, Lagrange basis).  Evaluated on the raw nodes; used by the
+ * tests as a second, independent route to the same coefficients. */
+int oracle_lagrange_row(const double *x, int n, double xstar, double *w) {
+  int rc = oracle_check_nodes(x, n);
+  if (rc) return rc;
+  for (int j = 0; j < n; ++j) {
+    double l = 1.0;
+    for (int k = 0; k < n; ++k)
+      if (k != j) l *= (xstar - x[k]) / (x[j] - x[k]);
+    w[j] = l;
+  }
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Exact decoding of storage formats (IEEE-754 definitions).                  */
+/* ------------------------------------------------------------------------ */
+
+/* bfloat16 is the upper half of an IEEE binary32 pattern. */
+double oracle_bf16_to_f64(uint16_t h) {
+  uint32_t u = (uint32_t)h << 16;
+  float f;
+  memcpy(&f, &u, sizeof f);
+  return (double)f;
+}
+
+/* Correct rounding of a binary64 value to bfloat16, ties to even, written
+ * from the format definition: 8 significand bits, exponent range of
+ * binary32 (normal down to 2^-126, subnormal spacing 2^-133). */
+uint16_t oracle_round_bf16(double v) {
+  if (isnan(v)) return (uint16_t)0x7FC0;
+  uint16_t sign = signbit(v) ? 0x8000 : 0x0000;
+  double a = fabs(v);
+  if (a == 0.0) return sign;
+  if (isinf(a)) return (uint16_t)(sign | 0x7F80);
+  int ex;
+  (void)frexp(a, &ex);          /* a = m * 2^ex, m in [0.5, 1) */
+  int e = ex - 1;               /* a in [2^e, 2^(e+1)) */
+  int qexp = (e < -126) ? -133 : e - 7;
+  double units = ldexp(a, -qexp);          /* exact: power-of-two scaling */
+  double r = floor(units);
+  double frac = units - r;                 /* exact: units < 2^9 */
+  if (frac > 0.5 || (frac == 0.5 && fmod(r, 2.0) != 0.0)) r += 1.0;
+  double rounded = ldexp(r, qexp);
+  if (rounded >= ldexp(1.0, 128)) return (uint16_t)(sign | 0x7F80);
+  float f = (float)rounded;                /* exact: fits in binary32 */
+  uint32_t u;
+  memcpy(&u, &f, sizeof u);
+  return (uint16_t)(sign | (uint16_t)((u >> 16) & 0x7FFF));
+}
+
+/* Correct rounding of binary64 to binary32, ties to even: the C cast under
+ * the default rounding mode is exactly that operation. */
+float oracle_round_f32(double v) { return (float)v; }
+
+/* Array forms of the two bfloat16 conversions. */
+void oracle_decode_bf16(const uint16_t *h, int64_t count, double *out) {
+  for (int64_t i = 0; i < count; ++i) out[i] = oracle_bf16_to_f64(h[i]);
+}
+
+void oracle_encode_bf16(const double *v, int64_t count, uint16_t *out) {
+  for (int64_t i = 0; i < count; ++i) out[i] = oracle_round_bf16(v[i]);
+}
+
+/* ------------------------------------------------------------------------ */
+/* The skipped-step prediction, element by element (Section 3.3, Alg. 1).    */
+/* ------------------------------------------------------------------------ */
+
+/* out[i] = sum_{k=0}^{n-1} w[k] * F_k[i], k from oldest to newest, fp64.
+ * When absmag is not NULL it receives sum_k |w[k]| * |F_k[i]|, the size of
+ * the terms that cancel, which the parity bound is stated against. */
+void oracle_extrapolate_bf16(const uint16_t *const *F, int n, const double *w,
+                             int64_t count, double *out, double *absmag) {
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < count; ++i) {
+    double s = 0.0, m = 0.0;
+    for (int k = 0; k < n; ++k) {
+      double f = oracle_bf16_to_f64(F[k][i]);
+      s += w[k] * f;
+      m += fabs(w[k]) * fabs(f);
+    }
+    out[i] = s;
+    if (absmag) absmag[i] = m;
+  }
+}
+
+void oracle_extrapolate_f32(const float *const *F, int n, const double *w,
+                            int64_t count, double *out, double *absmag) {
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < count; ++i) {
+    double s = 0.0, m = 0.0;
+    for (int k = 0; k < n; ++k) {
+      double f = (double)F[k][i];
+      s += w[k] * f;
+      m += fabs(w[k]) * fabs(f);
+    }
+    out[i] = s;
+    if (absmag) absmag[i] = m;
+  }
+}
+
+void oracle_extrapolate_f64(const double *const *F, int n, const double *w,
+                            int64_t count, double *out) {
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < count; ++i) {
+    double s = 0.0;
+    for (int k = 0; k < n; ++k) s += w[k] * F[k][i];
+    out[i] = s;
+  }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Full-computation schedule (Section 3.3, weight precomputation).           */
+/* ------------------------------------------------------------------------ */
+
+/* is_full[s] = 1 when step s of 0..T-1 runs the full network: s outside
+ * [s0, T-1-s1], or r divides (s - s0).  Returns the number of full steps. */
+int oracle_full_schedule(int T, int s0, int s1, int r, uint8_t *is_full) {
+  if (T < 1 || s0 < 0 || s1 < 0 || r < 1) return -1;
+  int count = 0;
+  for (int s = 0; s < T; ++s) {
+    int outside = (s < s0) || (s > T - 1 - s1);
+    int on_grid = ((s - s0) % r) == 0;
+    is_full[s] = (uint8_t)(outside || on_grid);
+    count += is_full[s];
+  }
+  return count;
+}

@@ -1,0 +1,100 @@
+"""The oracle's pins catch plausible mistakes.
+
+Each case plants one mistake in a copy of the oracle's C source (a wrong
+sign, a dropped term, a transposed or shifted index, a wrong rounding rule),
+builds it with gcc into a temporary library, points the oracle's Python
+binding at it and runs the pin battery of ``test_oracle_pins``; at least one
+pin must fail.  All on the CPU; the real oracle is restored afterwards.
+"""
+import functools
+import os
+import tempfile
+
+import pytest
+
+import oracle
+from oracle import build as oracle_build
+from tests import test_oracle_pins as pins
+
+# (name, text in oracle.c, replacement, which occurrence (0-based))
+MUTANTS = [
+    ("rho sign", "if (k != j) d *= (y[j] - y[k]);", "if (k != j) d *= (y[j] + y[k]);", 0),
+    ("rho drops factors", "if (k != j) d *= (y[j] - y[k]);",
+     "if (k > j) d *= (y[j] - y[k]);", 0),
+    ("denominator drops a term", "denom += q[j];", "if (j > 0) denom += q[j];", 0),
+    ("q multiplies", "q[j] = rho[j] / diff;", "q[j] = rho[j] * diff;", 0),
+    ("target mirrored", "*ystar = (2.0 * xstar - (a + b)) / (b - a);",
+     "*ystar = (2.0 * xstar - (a + b)) / (a - b);", 0),
+    ("target shifted", "*ystar = (2.0 * xstar - (a + b)) / (b - a);",
+     "*ystar = (2.0 * xstar - (a + a)) / (b - a);", 0),
+    ("node hit picks wrong slot", "w[k] = (k == j) ? 1.0 : 0.0;",
+     "w[k] = (k == 0) ? 1.0 : 0.0;", 0),
+    ("history order reversed (bf16)", "double f = oracle_bf16_to_f64(F[k][i]);",
+     "double f = oracle_bf16_to_f64(F[n - 1 - k][i]);", 0),
+    ("newest entry dropped (bf16)", "for (int k = 0; k < n; ++k) {\n      double f = oracle_bf16",
+     "for (int k = 0; k < n - 1; ++k) {\n      double f = oracle_bf16", 0),
+    ("magnitude keeps sign", "m += fabs(w[k]) * fabs(f);", "m += w[k] * fabs(f);", 0),
+    ("f32 decode drops oldest", "double f = (double)F[k][i];", "double f = (double)F[k ? k : 1][i];", 0),
+    ("f64 sum uses wrong index", "for (int k = 0; k < n; ++k) s += w[k] * F[k][i];",
+     "for (int k = 0; k < n; ++k) s += w[k] * F[k][i > 0 ? i - 1 : 0];", 0),
+    ("bf16 decode shift", "uint32_t u = (uint32_t)h << 16;", "uint32_t u = (uint32_t)h << 15;", 0),
+    ("ties to odd", "fmod(r, 2.0) != 0.0", "fmod(r, 2.0) == 0.0", 0),
+    ("nine significand bits", "int qexp = (e < -126) ? -133 : e - 7;",
+     "int qexp = (e < -126) ? -133 : e - 8;", 0),
+    ("rounding truncates", "if (frac > 0.5 ||", "if (frac > 1.5 ||", 0),
+    ("schedule end off by one", "(s > T - 1 - s1)", "(s > T - s1)", 0),
+    ("schedule grid offset", "((s - s0) % r) == 0", "((s - s0 + 1) % r) == 0", 0),
+]
+
+
+def _battery():
+    tests = []
+    for name in sorted(dir(pins)):
+        if not name.startswith("test_"):
+            continue
+        fn = getattr(pins, name)
+        if name == "test_config_weights_equal_exact_lagrange":
+            for case in pins._all_config_cases():
+                tests.append((f"{name}[{case[0]}]", functools.partial(fn, case)))
+        else:
+            tests.append((name, fn))
+    return tests
+
+
+def _replace_nth(text, old, new, n):
+    start = -1
+    for _ in range(n + 1):
+        start = text.index(old, start + 1)
+    return text[:start] + new + text[start + len(old):]
+
+
+@pytest.mark.parametrize("mutant", MUTANTS, ids=lambda m: m[0])
+def test_pins_catch_mutant(mutant, tmp_path):
+    name, old, new, nth = mutant
+    with open(oracle_build.SRC) as f:
+        src = f.read()
+    assert old in src, f"mutation site for {name!r} not found"
+    mutated = _replace_nth(src, old, new, nth)
+    path = os.path.join(tmp_path, "oracle_mutant.c")
+    with open(path, "w") as f:
+        f.write(mutated)
+    lib = oracle_build.build(src=path, out=os.path.join(tmp_path, "liboracle_mutant.so"))
+    saved = oracle.lib()
+    oracle._LIB = oracle.bind(lib)
+    caught = []
+    try:
+        for tname, fn in _battery():
+            try:
+                fn()
+            except (AssertionError, oracle.OracleError, ValueError, ZeroDivisionError,
+                    OverflowError):
+                caught.append(tname)
+                break
+    finally:
+        oracle._LIB = saved
+    assert caught, f"no pin failed for planted mistake {name!r}"
+
+
+def test_unmutated_oracle_passes_battery():
+    for tname, fn in _battery():
+        fn()

@@ -1,0 +1,350 @@
+"""Pins of the fp64 CPU oracle against what the paper and mathematics fix.
+
+Nothing here compares the oracle with itself: each check goes through an
+independent route (exact rational Lagrange coefficients, closed forms from
+Appendix A, the interpolation error theorem, a textbook finite-difference
+identity, format definitions checked by brute force, a library decoder).
+"""
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from synth import CONFIGS, make_history_f64
+from tests.lagrange_exact import lagrange_weights
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _all_config_cases():
+    for c in CONFIGS:
+        yield c.name, c.nodes, c.targets
+        if c.alt_nodes is not None:
+            yield c.name + "_alt", c.alt_nodes, c.alt_targets
+
+
+def _rand_nodes(rng, n, lo=-3.0, hi=5.0):
+    while True:
+        x = rng.uniform(lo, hi, size=n)
+        if n == 1 or np.min(np.diff(np.sort(x))) > 1e-3 * (hi - lo):
+            return x
+
+
+def _wtol(w, factor=4.0):
+    """Rounding bound for a weight row from the second barycentric form: the
+    denominator cancels down to 1/omega(x), so each weight carries a relative
+    error of order n u sum|w|, i.e. an absolute one of n u (sum|w|)^2."""
+    s = float(np.abs(w).sum())
+    return factor * len(w) * 2.0 ** -53 * s * max(s, 1.0)
+
+
+# --------------------------------------------------------------------------
+# Weights
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("case", list(_all_config_cases()), ids=lambda c: c[0])
+def test_config_weights_equal_exact_lagrange(case):
+    """Second barycentric form on normalised nodes == exact Lagrange basis."""
+    _, nodes, targets = case
+    w = oracle.weights(nodes, targets)
+    for m, t in enumerate(targets):
+        exact = lagrange_weights(nodes, t)
+        scale = float(sum(abs(e) for e in exact))
+        err = max(abs(w[m, j] - float(e)) for j, e in enumerate(exact))
+        assert err <= 1e-13 * scale, (t, w[m], [float(e) for e in exact])
+        assert sum(exact) == 1
+
+
+def test_tiny_weights_exact_fractions():
+    """Tiny workload, target 938: exact coefficients worked by hand from the
+    Lagrange basis on nodes 999, 979, 959, 939 (spacing -20, target at
+    offset 61/20 spacings): l_j = prod (3.05 - k) / (j - k)."""
+    w = oracle.weights([999, 979, 959, 939], [938])[0]
+    expect = [Fraction(-287, 16000), Fraction(1281, 16000), Fraction(-2501, 16000),
+              Fraction(17507, 16000)]
+    np.testing.assert_allclose(w, [float(e) for e in expect], rtol=0, atol=1e-15)
+
+
+def test_random_weights_equal_exact_lagrange():
+    rng = np.random.default_rng(7)
+    for n in range(1, 9):
+        for _ in range(20):
+            x = _rand_nodes(rng, n)
+            t = float(rng.uniform(-6, 8))
+            w = oracle.weights_row(x, t)
+            exact = lagrange_weights(x, t)
+            scale = float(sum(abs(e) for e in exact))
+            err = max(abs(w[j] - float(e)) for j, e in enumerate(exact))
+            # The second form's denominator sum_j rho_j/(x - x_j) cancels down
+            # to 1/omega(x); its relative rounding error, and so each weight's,
+            # grows like u * sum|w|.
+            assert err <= 4 * n * 2.0 ** -53 * scale * max(scale, 1.0), (n, x, t)
+
+
+def test_partition_of_unity():
+    """Appendix A: 1 = omega(x) sum_j rho_j / (x - x_j), i.e. sum_j w_j = 1."""
+    rng = np.random.default_rng(11)
+    for n in range(1, 9):
+        for _ in range(50):
+            x = _rand_nodes(rng, n)
+            w = oracle.weights_row(x, float(rng.uniform(-10, 10)))
+            assert abs(w.sum() - 1.0) <= _wtol(w)
+
+
+def test_target_at_node_is_unit_vector():
+    x = [0.96, 0.9, 0.8, 0.72, 0.6, 0.5]
+    for j, xj in enumerate(x):
+        w = oracle.weights_row(x, xj)
+        assert w.tolist() == [1.0 if k == j else 0.0 for k in range(len(x))]
+
+
+def test_single_node_is_reuse():
+    """K = 0: the interpolant is the constant through the one cached value."""
+    assert oracle.weights_row([500.0], 480.0).tolist() == [1.0]
+
+
+def test_equispaced_rho_matches_appendix():
+    """Appendix A: at equispaced nodes x_j = -1 + (j-1)h, h = 2/(N-1),
+    omega'(x_j) = h^(N-1) (j-1)! (-1)^(N-j) (N-j)!, and after dropping the
+    common factor rho_j = (-1)^(j-1) C(N-1, j-1) (golden table)."""
+    rows = {}
+    with open(os.path.join(GOLDEN, "equispaced_rho.txt")) as f:
+        for line in f:
+            if line.startswith("#") or not line.strip():
+                continue
+            vals = [int(v) for v in line.split()]
+            rows[vals[0]] = vals[1:]
+    assert sorted(rows) == list(range(1, 9))
+    for N, golden in rows.items():
+        if N == 1:
+            continue
+        h = 2.0 / (N - 1)
+        y = np.array([-1.0 + (j - 1) * h for j in range(1, N + 1)])
+        rho = oracle.barycentric_rho(y)
+        closed = np.array([1.0 / (h ** (N - 1) * math.factorial(j - 1) * (-1) ** (N - j)
+                                  * math.factorial(N - j)) for j in range(1, N + 1)])
+        np.testing.assert_allclose(rho, closed, rtol=1e-13)
+        ratio = rho / np.array(golden, dtype=np.float64)
+        np.testing.assert_allclose(ratio, ratio[0], rtol=1e-13)
+
+
+def test_normalisation_maps_span_to_unit_interval():
+    y, ys = oracle.normalise([999, 979, 959, 939], 919)
+    np.testing.assert_allclose(y, [1.0, 1 / 3, -1 / 3, -1.0], rtol=0, atol=1e-15)
+    assert abs(ys - (-5 / 3)) < 1e-15
+    y, ys = oracle.normalise([0.96, 0.9, 0.8, 0.72, 0.6, 0.5], 0.48)
+    assert y.min() == -1.0 and y.max() == 1.0 and ys < -1.0
+
+
+def test_one_step_ahead_equispaced_is_newton_difference():
+    """Textbook: for K+1 equispaced nodes the degree-K extrapolant one spacing
+    past the newest node has w_j = (-1)^(K-j) C(K+1, j) (the (K+1)-th forward
+    difference of a degree-K polynomial vanishes)."""
+    for K in range(0, 8):
+        x = [999.0 - 20.0 * j for j in range(K + 1)]
+        w = oracle.weights_row(x, 999.0 - 20.0 * (K + 1))
+        expect = [(-1) ** (K - j) * math.comb(K + 1, j) for j in range(K + 1)]
+        np.testing.assert_allclose(w, expect, rtol=0, atol=1e-12 * sum(map(abs, expect)))
+
+
+def test_affine_invariance():
+    """Lagrange coefficients do not depend on the affine frame of the nodes."""
+    rng = np.random.default_rng(3)
+    for n in range(2, 8):
+        x = _rand_nodes(rng, n)
+        t = float(rng.uniform(-6, 8))
+        w = oracle.weights_row(x, t)
+        for a, b in [(1000.0, 3.0), (-0.02, 1.0), (7.5, -250.0)]:
+            w2 = oracle.weights_row(a * x + b, a * t + b)
+            np.testing.assert_allclose(w2, w, rtol=0, atol=_wtol(w, 64.0))
+
+
+def test_permutation_equivariance():
+    rng = np.random.default_rng(5)
+    for n in range(2, 8):
+        x = _rand_nodes(rng, n)
+        t = float(rng.uniform(-6, 8))
+        w = oracle.weights_row(x, t)
+        p = rng.permutation(n)
+        np.testing.assert_allclose(oracle.weights_row(x[p], t), w[p], rtol=0,
+                                   atol=_wtol(w, 16.0))
+
+
+def test_lagrange_product_route_agrees():
+    rng = np.random.default_rng(9)
+    for n in range(1, 8):
+        x = _rand_nodes(rng, n)
+        t = float(rng.uniform(-6, 8))
+        w = oracle.lagrange_row(x, t)
+        np.testing.assert_allclose(oracle.weights_row(x, t), w, rtol=0, atol=_wtol(w, 16.0))
+
+
+def test_bad_nodes_rejected():
+    with pytest.raises(oracle.OracleError):
+        oracle.weights_row([1.0, 2.0, 1.0], 3.0)
+    with pytest.raises(oracle.OracleError):
+        oracle.weights_row([1.0, float("nan")], 3.0)
+    with pytest.raises(oracle.OracleError):
+        oracle.weights_row([1.0, 2.0], float("inf"))
+    with pytest.raises(oracle.OracleError):
+        oracle.weights_row([], 3.0)
+
+
+# --------------------------------------------------------------------------
+# The combination
+# --------------------------------------------------------------------------
+
+def test_polynomials_up_to_degree_K_reproduced():
+    """Appendix A error term f^(N)(xi)/N! omega(x) vanishes for degree <= N-1:
+    every element's own random polynomial of degree <= K comes back exactly."""
+    rng = np.random.default_rng(13)
+    E = 4096
+    for c in CONFIGS:
+        x = np.array(c.nodes)
+        for deg in range(0, c.K + 1):
+            coef = rng.standard_normal((deg + 1, E))
+            vals = np.stack([np.polynomial.polynomial.polyval(xk, coef) for xk in x])
+            for t in c.targets:
+                w = oracle.weights_row(x, t)
+                got = oracle.extrapolate_f64(list(vals), w)
+                want = np.polynomial.polynomial.polyval(t, coef)
+                mag = np.abs(w) @ np.abs(vals)
+                assert np.all(np.abs(got - want) <= 1e-12 * (mag + np.abs(want))), (c.name, deg, t)
+
+
+def test_error_theorem_for_monomial_of_degree_N():
+    """For f(x) = x^N with N nodes, f^(N)/N! = 1, so f(x) - P(x) = omega(x)."""
+    rng = np.random.default_rng(17)
+    for N in range(1, 8):
+        x = _rand_nodes(rng, N, -1.0, 1.0)
+        for t in rng.uniform(-2.5, 2.5, size=6):
+            w = oracle.weights_row(x, t)
+            P = oracle.extrapolate_f64([np.array([xk ** N]) for xk in x], w)[0]
+            omega = float(np.prod(t - x))
+            scale = np.abs(w) @ np.abs(x ** N) + abs(t) ** N + abs(omega)
+            tol = _wtol(w, 16.0) * np.max(np.abs(x ** N)) + 16 * N * 2.0 ** -53 * scale
+            assert abs((t ** N - P) - omega) <= tol, (N, t)
+
+
+def test_tiny_generator_linearity():
+    """Tiny workload: F_k = A + B tau_k + C tau_k^2 + 1e-3 eta_k (fp64, unrounded).
+    The K=3 combination returns the quadratic at the target exactly plus the
+    combined noise 1e-3 sum_k w_k eta_k."""
+    c = CONFIGS[0]
+    E = 20000
+    entries, coeffs, eta, taus = make_history_f64(c, E)
+    for t in list(c.targets) + list(c.alt_targets):
+        w = oracle.weights_row(c.nodes, t)
+        got = oracle.extrapolate_f64(list(entries), w)
+        tau = t / c.time_scale
+        want = coeffs[0] + coeffs[1] * tau + coeffs[2] * tau * tau + c.noise_std * (w @ eta)
+        mag = np.abs(w) @ np.abs(entries)
+        assert np.all(np.abs(got - want) <= 1e-13 * (mag + 1.0))
+
+
+def test_extrapolate_bf16_decodes_and_reports_magnitude():
+    rng = np.random.default_rng(19)
+    n, E = 6, 3001
+    vals = rng.standard_normal((n, E)).astype(np.float32)
+    bits = [torch.from_numpy(v).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+            for v in vals]
+    dec = np.stack([torch.from_numpy(b.view(np.int16)).view(torch.bfloat16).double().numpy()
+                    for b in bits])
+    w = oracle.weights_row([2, 5, 10, 14, 20, 25], 27)
+    out, mag = oracle.extrapolate_bf16(bits, w)
+    ref = np.zeros(E)
+    for k in range(n):            # written out: oldest to newest, fp64
+        ref = ref + w[k] * dec[k]
+    np.testing.assert_array_equal(out, ref)
+    np.testing.assert_allclose(mag, np.abs(w) @ np.abs(dec), rtol=1e-15)
+
+
+def test_extrapolate_f32_exact_decode():
+    rng = np.random.default_rng(23)
+    vals = rng.standard_normal((4, 1000)).astype(np.float32)
+    w = np.array([-1.0, 4.0, -6.0, 4.0])
+    out, _ = oracle.extrapolate_f32(list(vals), w)
+    ref = (((w[0] * vals[0].astype(np.float64)) + w[1] * vals[1].astype(np.float64))
+           + w[2] * vals[2].astype(np.float64)) + w[3] * vals[3].astype(np.float64)
+    np.testing.assert_array_equal(out, ref)
+
+
+# --------------------------------------------------------------------------
+# Storage formats
+# --------------------------------------------------------------------------
+
+def test_bf16_decode_all_patterns_matches_torch():
+    bits = np.arange(65536, dtype=np.uint16)
+    mine = oracle.bf16_to_f64(bits)
+    ref = torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).double().numpy()
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(mine), nan)
+    assert np.array_equal(mine[~nan], ref[~nan])
+    assert np.array_equal(np.signbit(mine[~nan]), np.signbit(ref[~nan]))
+
+
+def _decode(b):
+    return oracle.bf16_to_f64(np.array([b], dtype=np.uint16))[0]
+
+
+def test_round_bf16_is_nearest_ties_to_even():
+    """Brute force over neighbours: the chosen pattern is the nearest finite
+    bfloat16, and on an exact tie it has an even last significand bit."""
+    rng = np.random.default_rng(29)
+    exps = rng.integers(-140, 128, size=3000)
+    v = rng.uniform(1.0, 2.0, size=3000) * np.ldexp(1.0, exps) * rng.choice([-1, 1], 3000)
+    ties = np.array([_decode(b) for b in range(0x3F80, 0x3F90)])
+    mids = (ties[:-1] + ties[1:]) / 2            # exact midpoints
+    v = np.concatenate([v, mids, -mids, [0.0, -0.0, 1e-50, 3.0e38, 3.4e38]])
+    got = oracle.round_bf16(v)
+    for x, b in zip(v, got):
+        b = int(b)
+        d = _decode(b)
+        if math.isinf(d):
+            assert abs(x) >= 3.3895313892515355e38  # past the largest finite + half ulp
+            continue
+        cand = [c for c in ((b - 1) & 0xFFFF, (b + 1) & 0xFFFF) if (c & 0x7F80) != 0x7F80]
+        for c in cand:
+            dc = _decode(c)
+            assert abs(x - d) <= abs(x - dc), (x, hex(b), hex(c))
+            if abs(x - d) == abs(x - dc) and dc != d:
+                assert b % 2 == 0, (x, hex(b))
+    # the midpoints between consecutive patterns go to the even one
+    for m, lo in zip(mids, range(0x3F80, 0x3F8F)):
+        assert int(oracle.round_bf16([m])[0]) == (lo if lo % 2 == 0 else lo + 1)
+
+
+def test_round_bf16_agrees_with_torch_on_f32_inputs():
+    """torch's float32 -> bfloat16 is round-to-nearest-even; for inputs that
+    are already binary32 the single rounding must agree."""
+    rng = np.random.default_rng(31)
+    v32 = (rng.standard_normal(200000) * np.exp(rng.uniform(-30, 30, 200000))).astype(np.float32)
+    mine = oracle.round_bf16(v32.astype(np.float64))
+    ref = torch.from_numpy(v32).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(mine, ref)
+
+
+# --------------------------------------------------------------------------
+# Schedule
+# --------------------------------------------------------------------------
+
+def test_full_schedule_golden():
+    with open(os.path.join(GOLDEN, "full_schedule.txt")) as f:
+        lines = [l.split("#")[0].strip() for l in f]
+    n = 0
+    for line in lines:
+        if not line:
+            continue
+        head, tail = line.split(":")
+        kind, T, s0, s1, r = head.split()
+        mask = oracle.full_schedule(int(T), int(s0), int(s1), int(r))
+        if kind == "set":
+            assert np.flatnonzero(mask).tolist() == [int(v) for v in tail.split()], line
+        else:
+            assert int(mask.sum()) == int(tail), line
+        n += 1
+    assert n == 9
