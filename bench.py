@@ -1,0 +1,310 @@
+#!/usr/bin/env python3
+"""Benchmark of the ChebBooster online stage on one MI355X.
+
+A step is one skipped diffusion step: readiness check and weight row for the
+target (host, fp64) plus the prediction of every cached module output (one
+launch of the streaming kernel) over the FLUX.1-dev 1024x1024 feature cache
+(19 x [1,4096,3072] + 19 x [1,512,3072] + 38 x [1,4608,3072] bf16, six
+history entries).  Inputs are seeded synthetic features already resident in
+HBM.  The history is filled once before timing through the full-step push,
+which is timed on its own and reported beside the step.
+
+Prints one JSON line.  Throughput counts algorithmic bytes: (K+1) entries read
+plus one output written, per step.
+"""
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "achieved HBM GB/s and µs per skipped step, FLUX-1024 cache shape, 1 MI355X"
+PEAK_HBM_GBPS = 8000.0
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2608_23429_amd", "csrc", "kernels.hip")
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def kernel_sha256():
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def measured_traffic(workload):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if they
+    were taken on the current kernel source; else None."""
+    path = os.path.join(PROFILES, f"traffic_extrapolate_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    sha = re.search(r"kernel_source_sha256:\s*([0-9a-f]{64})", text)
+    val = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not sha or not val or sha.group(1) != kernel_sha256():
+        return None
+    return float(val.group(1))
+
+
+def parse_args(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="flux_dev_1024")
+    ap.add_argument("--unroll", type=int, default=None)
+    ap.add_argument("--nontemporal", type=int, default=None)
+    ap.add_argument("--blocks-per-cu", type=int, default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="approximate CPU time budget of the oracle baseline")
+    ap.add_argument("--other-configs", action="store_true",
+                    help="also time the other four workloads (reported under per_config)")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="only run a plain device copy of known size (counter calibration)")
+    return ap.parse_args(argv)
+
+
+def copy_probe(torch):
+    nbytes = 2 << 30
+    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record()
+    for _ in range(10):
+        dst.copy_(src)
+    e.record()
+    e.synchronize()
+    ms = s.elapsed_time(e) / 10
+    print(json.dumps({"copy_probe_bytes_read": nbytes, "copy_probe_bytes_written": nbytes,
+                      "ms": ms, "gbps": 2 * nbytes / ms / 1e6}), flush=True)
+
+
+def setup_workload(torch, cheb, cfg):
+    """Seeded history on the device, pushed through the ring."""
+    from synth import make_history, split_segments
+    dt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    t0 = time.time()
+    entries = make_history(cfg, "cuda")
+    torch.cuda.synchronize()
+    log(f"[bench] {cfg.name}: generated {cfg.n_hist} x {cfg.numel} elements "
+        f"in {time.time() - t0:.1f} s")
+    cache = cheb.ChebCache(cfg.n_hist, dt, cfg.seg_numel)
+    stream = torch.cuda.current_stream()
+    push_ms = []
+    for x, e in zip(cfg.nodes, entries):
+        s, f = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record(stream)
+        cache.push(x, split_segments(e, cfg))
+        f.record(stream)
+        f.synchronize()
+        push_ms.append(s.elapsed_time(f))
+    return entries, cache, push_ms
+
+
+def time_steps(torch, cache, targets, out, steps, warmup):
+    """Whole-region and per-launch HIP-event timing of `steps` skipped steps
+    on torch's current stream (the stream the kernel is launched on)."""
+    stream = torch.cuda.current_stream()
+    for i in range(warmup):
+        cache.extrapolate_at(targets[i % len(targets)], out, stream=stream)
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for i in range(steps):
+        cache.extrapolate_at(targets[i % len(targets)], out, stream=stream)
+    end.record(stream)
+    end.synchronize()
+    region_ms = start.elapsed_time(end) / steps
+    # per-launch durations, same stream, events right around each launch
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(steps)]
+    for i, (a, b) in enumerate(evs):
+        a.record(stream)
+        cache.extrapolate_at(targets[i % len(targets)], out, stream=stream)
+        b.record(stream)
+    torch.cuda.synchronize()
+    per = sorted(a.elapsed_time(b) for a, b in evs)
+    return region_ms, per
+
+
+def parity_sample(torch, cfg, entries, cache, out, target, count=1 << 16):
+    import numpy as np
+    import oracle
+    idx = np.unique(np.random.default_rng(cfg.seed).integers(0, cfg.numel, count))
+    it = torch.from_numpy(idx).to("cuda")
+    cache.extrapolate_at(target, out)
+    torch.cuda.synchronize()
+    w = oracle.weights_row(cfg.nodes, target)
+    if cfg.dtype == "bf16":
+        hosts = [e.index_select(0, it).view(torch.int16).cpu().numpy().view(np.uint16)
+                 for e in entries]
+        exp, mag = oracle.extrapolate_bf16(hosts, w)
+        got = oracle.bf16_to_f64(out.index_select(0, it).view(torch.int16).cpu().numpy()
+                                 .view(np.uint16))
+    else:
+        hosts = [e.index_select(0, it).cpu().numpy() for e in entries]
+        exp, mag = oracle.extrapolate_f32(hosts, w)
+        got = out.index_select(0, it).cpu().numpy().astype(np.float64)
+    err = oracle.parity_error(got, exp, mag)
+    return {"samples": int(idx.size), "floored_rel_err": err[0], "normwise_err": err[2],
+            "bound": 1e-2 if cfg.dtype == "bf16" else 1e-5}
+
+
+def cpu_baseline(torch, cfg, entries, target, seconds):
+    """The oracle, as it stands, on a bounded leading slice of every entry."""
+    import numpy as np
+    import oracle
+    try:
+        cores = len(os.sched_getaffinity(0))
+    except AttributeError:
+        cores = os.cpu_count() or 1
+    threads = oracle.set_threads(min(cores, int(os.environ.get("OMP_NUM_THREADS", cores))))
+    w = oracle.weights_row(cfg.nodes, target)
+
+    def host_slice(n):
+        if cfg.dtype == "bf16":
+            return [e[:n].view(torch.int16).cpu().numpy().view(np.uint16) for e in entries]
+        return [e[:n].cpu().numpy() for e in entries]
+
+    def run(hosts):
+        t0 = time.perf_counter()
+        if cfg.dtype == "bf16":
+            oracle.extrapolate_bf16(hosts, w, want_absmag=False)
+        else:
+            oracle.extrapolate_f32(hosts, w, want_absmag=False)
+        return time.perf_counter() - t0
+
+    n0 = min(cfg.numel, 1 << 22)
+    t0 = run(host_slice(n0))
+    n = int(min(cfg.numel, max(n0, n0 * seconds / max(t0, 1e-6))))
+    hosts = host_slice(n)
+    dt = run(hosts)
+    bytes_alg = (cfg.n_hist + 1) * n * cfg.elem_size
+    return {"value": bytes_alg / dt / 1e9, "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "seconds": dt, "us_per_step_scaled": dt * 1e6 * cfg.numel / n,
+            "sample": f"first {n} of {cfg.numel} elements of each of the {cfg.n_hist} "
+                      f"history entries, one target (t={target}); value counts the same "
+                      f"algorithmic bytes per element as the GPU step"}
+
+
+def measure_config(torch, cheb, cfg, steps, warmup):
+    entries, cache, push_ms = setup_workload(torch, cheb, cfg)
+    out = cache.new_output()
+    region_ms, per = time_steps(torch, cache, cfg.targets, out, steps, warmup)
+    avg_launch_ms = sum(per) / len(per)
+    B = cfg.bytes_per_step
+    res = {
+        "workload": cfg.name, "elements": cfg.numel, "history": cfg.n_hist, "dtype": cfg.dtype,
+        "bytes_per_step": B, "us_per_step": region_ms * 1e3,
+        "gbps": B / (region_ms * 1e6), "frac_of_8tbps": B / (region_ms * 1e6) / PEAK_HBM_GBPS,
+        "launch_us_median": per[len(per) // 2] * 1e3, "launch_us_p10": per[len(per) // 10] * 1e3,
+        "launch_us_p90": per[(9 * len(per)) // 10] * 1e3, "launch_us_avg": avg_launch_ms * 1e3,
+        "push_us_median": sorted(push_ms)[len(push_ms) // 2] * 1e3,
+        "push_gbps": 2 * cfg.numel * cfg.elem_size / (sorted(push_ms)[len(push_ms) // 2] * 1e6),
+    }
+    return res, entries, cache, out
+
+
+def main(argv=None):
+    args = parse_args(argv)
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: the skipped-step prediction needs no "
+              "communication, and this build runs on a single MI355X. Run with --gpus 1.",
+              file=sys.stderr, flush=True)
+        return 2
+    import torch
+    import paper_2608_23429_amd as cheb
+    from synth import by_name
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 1
+    torch.cuda.set_device(0)
+    if args.copy_probe:
+        copy_probe(torch)
+        return 0
+
+    shape = cheb.cheb_get_launch_config()
+    for k, v in (("unroll", args.unroll), ("nontemporal", args.nontemporal),
+                 ("blocks_per_cu", args.blocks_per_cu)):
+        if v is not None:
+            shape[k] = v
+    cheb.cheb_set_launch_config(**shape)
+
+    cfg = by_name(args.config)
+    log(f"[bench] workload {cfg.name}, launch shape {shape}, "
+        f"{args.warmup} warmup + {args.steps} timed steps")
+    res, entries, cache, out = measure_config(torch, cheb, cfg, args.steps, args.warmup)
+    log(f"[bench] {cfg.name}: {res['us_per_step']:.1f} us/step, {res['gbps']:.0f} GB/s")
+    par = parity_sample(torch, cfg, entries, cache, out, cfg.targets[-1])
+    log(f"[bench] parity sample: floored error {par['floored_rel_err']:.3e}")
+    achieved = res["bytes_per_step"] / (res["launch_us_avg"] * 1e3)
+    traffic = measured_traffic(cfg.name)
+    line = {
+        "metric": METRIC,
+        "value": res["gbps"],
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": res["us_per_step"] / 1e3,
+        "us_per_step": res["us_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if cfg.dtype == "bf16" else "f32",
+        "data": "synthetic: seeded per-element random polynomial in the time variable plus "
+                "Gaussian noise, stored in the cache dtype",
+        "config": {"workload": cfg.name, "elements_per_entry": cfg.numel,
+                   "history_entries": cfg.n_hist, "segments": len(cfg.segments),
+                   "bytes_per_step": res["bytes_per_step"], "launch": shape,
+                   "parallelism": "single GPU"},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBPS,
+                     "unit": "GB/s", "frac": achieved / PEAK_HBM_GBPS, "traffic": traffic},
+        "launch_us": {"median": res["launch_us_median"], "p10": res["launch_us_p10"],
+                      "p90": res["launch_us_p90"], "avg": res["launch_us_avg"]},
+        "push": {"us_median": res["push_us_median"], "gbps": res["push_gbps"],
+                 "note": "full-step copy into the ring, once per full step (not in value)"},
+        "parity_sample": par,
+    }
+    if not args.no_cpu_baseline:
+        log(f"[bench] oracle CPU baseline (~{args.cpu_seconds:.0f} s)")
+        line["cpu_baseline"] = cpu_baseline(torch, cfg, entries, cfg.targets[-1],
+                                            args.cpu_seconds)
+        log(f"[bench] oracle: {line['cpu_baseline']['value']:.2f} GB/s on "
+            f"{line['cpu_baseline']['cores']} threads")
+    cache.close()
+    del entries, cache, out
+    torch.cuda.empty_cache()
+    if args.other_configs:
+        from synth import CONFIGS
+        per = []
+        for c in CONFIGS:
+            if c.name == cfg.name:
+                continue
+            r, e, ch, o = measure_config(torch, cheb, c, max(10, args.steps // 2), args.warmup)
+            log(f"[bench] {c.name}: {r['us_per_step']:.1f} us/step, {r['gbps']:.0f} GB/s")
+            per.append(r)
+            ch.close()
+            del e, ch, o
+            torch.cuda.empty_cache()
+        line["per_config"] = per
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,248 @@
+/*
+ * cheb.h: C ABI of libcheb, the ChebBooster online stage on AMD MI355X
+ * (gfx950).
+ *
+ * ChebBooster skips a diffusion-transformer forward pass at some steps.  On
+ * such a step it predicts every cached module output as a fixed linear
+ * combination of the last n = K+1 fully computed ones:
+ *
+ *     f_t = sum_j w_t^j f_{s_j}   (paper, Section 3.3, forward application;
+ *                                   Algorithm 1, online stage)
+ *
+ * The weights w_t^j are Lagrange interpolation coefficients in barycentric
+ * form (Section 3.2, coefficient equation; Appendix A, general weights and
+ * second form).  They depend only on the history abscissae and the target,
+ * so they are computed once on the host in fp64 (Section 3.3, weight
+ * precomputation).  The per-step work is a streaming weighted sum over every
+ * cached tensor, run here as one HIP launch.
+ *
+ * Conventions for every call
+ *   - Return value: CHEB_OK (0) or a negative cheb_status.  On failure,
+ *     cheb_last_error() returns a message for the calling thread.  Every
+ *     argument is checked on the host before anything is enqueued, so a
+ *     failed call has enqueued no GPU work.
+ *   - Device memory (history arena, sources, outputs) belongs to the caller.
+ *     The library never allocates or frees device memory.  It owns only the
+ *     host-side handle returned by cheb_cache_create.
+ *   - `stream` is a hipStream_t passed as void*.  NULL means the default
+ *     stream.  GPU work is asynchronous on that stream.  Calls enqueue work in
+ *     program order; the caller orders work across streams.
+ *   - History order is always oldest to newest.
+ *   - Storage types: CHEB_BF16 (bfloat16) storage with fp32 accumulation and
+ *     round-to-nearest-even output; CHEB_F32 (binary32) storage with fp64
+ *     accumulation and round-to-nearest-even output.
+ *   - Distinct cache handles may be used from different threads at once.  One
+ *     handle must not be used by two threads at the same time.
+ */
+#ifndef CHEB_H
+#define CHEB_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define CHEB_VERSION 1
+
+#if defined(__GNUC__) || defined(__clang__)
+#define CHEB_API __attribute__((visibility("default")))
+#else
+#define CHEB_API
+#endif
+
+/* Largest history (K+1) the device kernels take. */
+#define CHEB_MAX_SLOTS 8
+/* Largest node count cheb_precompute_weights takes. */
+#define CHEB_MAX_NODES 64
+
+typedef enum cheb_status {
+  CHEB_OK = 0,
+  CHEB_E_INVAL = -1,     /* null pointer, count or enum out of range */
+  CHEB_E_DUPNODE = -2,   /* two equal history abscissae */
+  CHEB_E_NOTREADY = -3,  /* history holds fewer than n entries, or a push is open */
+  CHEB_E_DTYPE = -4,     /* unknown storage type */
+  CHEB_E_ALIGN = -5,     /* device pointer not aligned as documented */
+  CHEB_E_HIP = -6,       /* the HIP runtime reported an error */
+  CHEB_E_MISMATCH = -7,  /* sizes disagree (arena too small, ...) */
+  CHEB_E_NONFINITE = -8  /* NaN or infinite abscissa or weight */
+} cheb_status;
+
+typedef enum cheb_dtype { CHEB_BF16 = 0, CHEB_F32 = 1 } cheb_dtype;
+
+/* Message for the last failed call on this thread ("" if none).  The
+ * pointer stays valid until the next failing call on the same thread. */
+CHEB_API const char *cheb_last_error(void);
+
+/* CHEB_VERSION of the built library. */
+CHEB_API int cheb_version(void);
+
+/* ------------------------------------------------------------------------ */
+/* Weight precomputation (host, fp64).                                       */
+/* ------------------------------------------------------------------------ */
+
+/* Interpolation coefficients of the degree-(n_hist-1) polynomial through the
+ * history abscissae, evaluated at each target (Section 3.2, coefficient
+ * equation; Appendix A, rho_j = 1/omega'(x_j) and second barycentric form;
+ * Section 3.3, nodes and target mapped affinely onto [-1, 1]).
+ *
+ *   hist_t   [n_hist] host fp64: history abscissae (timesteps or sigma),
+ *            oldest to newest, finite and pairwise distinct.
+ *   target_t [n_target] host fp64: finite targets.  A target equal to a
+ *            history abscissa gets the unit row of that entry.
+ *   w_out    [n_target][n_hist] host fp64, row-major, caller-owned.  Row m
+ *            sums to 1 up to rounding.
+ *
+ * 1 <= n_hist <= CHEB_MAX_NODES, n_target >= 0.  Errors: CHEB_E_INVAL,
+ * CHEB_E_NONFINITE, CHEB_E_DUPNODE.  w_out is not written on error. */
+CHEB_API int cheb_precompute_weights(const double *hist_t, int32_t n_hist,
+                            const double *target_t, int32_t n_target,
+                            double *w_out);
+
+/* ------------------------------------------------------------------------ */
+/* Stateless combination.                                                    */
+/* ------------------------------------------------------------------------ */
+
+/* out[i] = sum_{k=0}^{n_src-1} w[k] * src[k][i] for 0 <= i < numel
+ * (Section 3.3, forward application), in one launch.
+ *
+ *   src     [n_src] host array of device pointers, each to numel elements of
+ *           `dtype`, 16-byte aligned.
+ *   w       [n_src] host fp64 weights (converted to fp32 on the bf16 path).
+ *   out     device pointer to numel elements of `dtype`, 16-byte aligned.
+ *           It may not overlap any source.
+ *   numel   >= 0, below 2^34.  Any value; a ragged tail is handled.
+ *
+ * 1 <= n_src <= CHEB_MAX_SLOTS.  Errors: CHEB_E_INVAL, CHEB_E_DTYPE,
+ * CHEB_E_ALIGN, CHEB_E_NONFINITE, CHEB_E_HIP. */
+CHEB_API int cheb_combine(const void *const *src, int32_t n_src, const double *w,
+                 void *out, int64_t numel, int32_t dtype, void *stream);
+
+/* ------------------------------------------------------------------------ */
+/* History cache: a ring of n entries in one caller-owned device arena.      */
+/* ------------------------------------------------------------------------ */
+
+/* The fixed-size history buffer H of (abscissa, features) pairs holding the
+ * n most recent full steps; a push into a full buffer evicts the oldest
+ * (Section 3.3, forward application; Algorithm 1, online stage).
+ *
+ * Layout.  One entry ("slot") holds every cached tensor ("segment") of one
+ * full step, back to back.  Segment s starts at element seg_offset[s], with
+ * offsets rounded up to 16 bytes (8 bf16 or 4 fp32 elements).  Elements
+ * between segments are padding.  slot_numel is the end of the last segment,
+ * rounded up the same way.  Slots are slot_stride_bytes apart (a multiple of
+ * 256) from the start of the arena.  Outputs of cheb_extrapolate use the same
+ * flat layout: segment s of the prediction is at out + seg_offset[s]. */
+typedef struct cheb_cache cheb_cache;
+
+/* Layout of a cache without creating it.
+ *   seg_numel  [n_segs] element counts (each >= 0).
+ *   seg_offset [n_segs] out, may be NULL.
+ *   slot_numel, slot_stride_bytes, arena_bytes: out, each may be NULL.
+ * 1 <= n_slots <= CHEB_MAX_SLOTS, n_segs >= 1.  Errors: CHEB_E_INVAL,
+ * CHEB_E_DTYPE. */
+CHEB_API int cheb_cache_layout(int32_t n_slots, int32_t dtype, const int64_t *seg_numel,
+                      int32_t n_segs, int64_t *seg_offset, int64_t *slot_numel,
+                      size_t *slot_stride_bytes, size_t *arena_bytes);
+
+/* Creates a handle over `arena` (device, 256-byte aligned, at least
+ * arena_bytes of cheb_cache_layout).  The arena stays caller-owned and must
+ * outlive the handle.  The history starts empty.  Errors: CHEB_E_INVAL,
+ * CHEB_E_DTYPE, CHEB_E_ALIGN, CHEB_E_MISMATCH. */
+CHEB_API int cheb_cache_create(cheb_cache **out, int32_t n_slots, int32_t dtype,
+                      const int64_t *seg_numel, int32_t n_segs, void *arena,
+                      size_t arena_bytes);
+
+/* Frees the handle (not the arena).  NULL is accepted. */
+CHEB_API int cheb_cache_destroy(cheb_cache *c);
+
+/* Empties the history (metadata only; arena contents are left as they are). */
+CHEB_API int cheb_cache_reset(cheb_cache *c);
+
+/* Stores the full step at abscissa t: copies segment s from seg_src[s]
+ * (device, 16-byte aligned, seg_numel[s] elements) into the slot of the
+ * oldest entry (or the next free one), zero-fills the padding after each
+ * segment, records t and advances the ring (Algorithm 1, full computation:
+ * store (s, f_s) in H).  One launch per 64 segments, asynchronous on
+ * `stream`.  Errors: CHEB_E_INVAL, CHEB_E_NONFINITE, CHEB_E_DUPNODE (t already
+ * held), CHEB_E_ALIGN, CHEB_E_NOTREADY (a fused push is open), CHEB_E_HIP. */
+CHEB_API int cheb_cache_push(cheb_cache *c, double t, const void *const *seg_src,
+                    void *stream);
+
+/* Fused push, part 1: returns in *slot_base the device address of the slot
+ * the next entry will occupy, so the full step can write its outputs there
+ * directly (segment s at slot_base + seg_offset[s] elements).  The entry that
+ * slot held is dropped from the history at once.  Until cheb_cache_commit,
+ * pushes and extrapolations fail with CHEB_E_NOTREADY.  Errors: CHEB_E_INVAL,
+ * CHEB_E_NOTREADY (already open). */
+CHEB_API int cheb_cache_begin_push(cheb_cache *c, void **slot_base);
+
+/* Fused push, part 2: records abscissa t for the open slot (metadata only;
+ * no GPU work).  The caller orders the writes into the slot before any later
+ * use of the cache on its streams.  Errors: CHEB_E_INVAL, CHEB_E_NONFINITE,
+ * CHEB_E_DUPNODE, CHEB_E_NOTREADY (no push open). */
+CHEB_API int cheb_cache_commit(cheb_cache *c, double t);
+
+/* Abscissae held, oldest to newest: t_out[0 .. *count-1] (t_out has room for
+ * n_slots values; it may be NULL).  Errors: CHEB_E_INVAL. */
+CHEB_API int cheb_cache_history(const cheb_cache *c, double *t_out, int32_t *count);
+
+/* Device address of the entry of age index `idx` (0 = oldest held).
+ * Errors: CHEB_E_INVAL (idx outside 0 .. count-1). */
+CHEB_API int cheb_cache_entry(const cheb_cache *c, int32_t idx, void **slot_base);
+
+/* Element offset of segment `seg` in a slot and in an output buffer. */
+CHEB_API int cheb_cache_segment_offset(const cheb_cache *c, int32_t seg,
+                              int64_t *elem_offset);
+
+/* Elements of one slot (= elements an output buffer must hold). */
+CHEB_API int cheb_cache_slot_numel(const cheb_cache *c, int64_t *numel);
+
+/* The skipped-step prediction (Section 3.3, forward application equation;
+ * Algorithm 1, extrapolation branch):
+ *     out[i] = sum_{k=0}^{n-1} w[k] * H_k[i],  H_0 oldest .. H_{n-1} newest,
+ * over every element of every segment, in one launch.
+ *   w    [n_slots] host fp64, aligned with cheb_cache_history's order (for
+ *        example a row of cheb_precompute_weights over those abscissae).
+ *   out  device, 16-byte aligned, cheb_cache_slot_numel elements, not
+ *        overlapping the arena.  Padding elements of out are unspecified.
+ * Requires a full history (|H| = n; Section 3.3).  Errors: CHEB_E_INVAL,
+ * CHEB_E_NOTREADY, CHEB_E_ALIGN, CHEB_E_NONFINITE, CHEB_E_HIP. */
+CHEB_API int cheb_extrapolate(cheb_cache *c, const double *w, void *out, void *stream);
+
+/* Readiness check, weight row and prediction in one call: computes the fp64
+ * coefficients of the held abscissae at `target_t` (as
+ * cheb_precompute_weights) and runs cheb_extrapolate with them.  The weights
+ * used can be read back through w_used ([n_slots] host fp64, may be NULL).
+ * Errors: those of cheb_precompute_weights and cheb_extrapolate. */
+CHEB_API int cheb_extrapolate_at(cheb_cache *c, double target_t, void *out,
+                        void *stream, double *w_used);
+
+/* ------------------------------------------------------------------------ */
+/* Launch shape (tuning).                                                    */
+/* ------------------------------------------------------------------------ */
+
+/* Launch shape of the streaming kernels, process-wide.
+ *   unroll       16-byte vectors per thread per history entry in flight
+ *                (1, 2 or 4).
+ *   nontemporal  1: history loads and output stores carry the non-temporal
+ *                hint; 0: ordinary loads and stores.
+ *   blocks_per_cu  0: one block per tile of 256 x unroll vectors (the grid
+ *                covers the whole problem); > 0: a persistent grid of that
+ *                many blocks per compute unit, each looping over tiles.
+ * Errors: CHEB_E_INVAL. */
+typedef struct cheb_launch_config {
+  int32_t unroll;
+  int32_t nontemporal;
+  int32_t blocks_per_cu;
+} cheb_launch_config;
+
+CHEB_API int cheb_get_launch_config(cheb_launch_config *cfg);
+CHEB_API int cheb_set_launch_config(const cheb_launch_config *cfg);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CHEB_H */

@@ -1,0 +1,183 @@
+"""ChebBooster online stage on AMD MI355X (gfx950).
+
+``libcheb.so`` (C ABI in ``include/cheb.h``) does all the work: fp64 host
+weights, the device history ring, the full-step push and the skipped-step
+prediction kernel.  This package is its Python face: the C entry points under
+their own names (``_binding``) and a small tensor-level wrapper,
+``ChebCache``, that takes torch tensors and streams and passes their
+addresses through.  PyTorch provides device memory and streams only.
+"""
+from typing import List, Optional, Sequence
+
+import numpy as np
+import torch
+
+from ._binding import (  # noqa: F401  (re-exported C entry points)
+    CHEB_BF16, CHEB_F32, CHEB_MAX_NODES, CHEB_MAX_SLOTS, ChebError,
+    cheb_cache_begin_push, cheb_cache_commit, cheb_cache_create, cheb_cache_destroy,
+    cheb_cache_entry, cheb_cache_history, cheb_cache_layout, cheb_cache_push,
+    cheb_cache_reset, cheb_cache_segment_offset, cheb_cache_slot_numel, cheb_combine,
+    cheb_extrapolate, cheb_extrapolate_at, cheb_get_launch_config, cheb_last_error,
+    cheb_precompute_weights, cheb_set_launch_config, cheb_version,
+)
+from . import _binding
+
+LIB_PATH = _binding.LIB_PATH
+
+_DTYPES = {torch.bfloat16: CHEB_BF16, torch.float32: CHEB_F32}
+_TORCH = {CHEB_BF16: torch.bfloat16, CHEB_F32: torch.float32}
+
+
+def cheb_dtype(dtype: torch.dtype) -> int:
+    try:
+        return _DTYPES[dtype]
+    except KeyError:
+        raise ChebError(_binding.CHEB_E_DTYPE, f"unsupported dtype {dtype}") from None
+
+
+def _stream_handle(stream: Optional[torch.cuda.Stream]) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return int(stream.cuda_stream)
+
+
+def _check_device_tensor(t: torch.Tensor, what: str):
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ChebError(_binding.CHEB_E_INVAL, f"{what} must be a GPU tensor")
+    if not t.is_contiguous():
+        raise ChebError(_binding.CHEB_E_INVAL, f"{what} must be contiguous")
+
+
+def combine(srcs: Sequence[torch.Tensor], w, out: torch.Tensor,
+            stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+    """out = sum_k w[k] * srcs[k] (elementwise, one launch of cheb_combine)."""
+    if len(srcs) == 0:
+        raise ChebError(_binding.CHEB_E_INVAL, "no sources")
+    dt = cheb_dtype(out.dtype)
+    _check_device_tensor(out, "out")
+    for i, s in enumerate(srcs):
+        _check_device_tensor(s, f"srcs[{i}]")
+        if s.dtype != out.dtype or s.numel() != out.numel():
+            raise ChebError(_binding.CHEB_E_MISMATCH, f"srcs[{i}] differs from out in dtype or size")
+    cheb_combine([s.data_ptr() for s in srcs], w, out.data_ptr(), out.numel(), dt,
+                 _stream_handle(stream))
+    return out
+
+
+def precompute_weights(hist_t, target_t) -> np.ndarray:
+    return cheb_precompute_weights(hist_t, target_t)
+
+
+class ChebCache:
+    """The history ring of one feature set, over a torch-allocated arena.
+
+    ``seg_numel`` lists the element counts of the cached tensors in cache
+    order.  Outputs and slots share one flat layout; ``segment_views``
+    cuts a flat buffer into per-segment views.
+    """
+
+    def __init__(self, n_slots: int, dtype: torch.dtype, seg_numel: Sequence[int],
+                 device=None, arena: Optional[torch.Tensor] = None):
+        self.n_slots = int(n_slots)
+        self.dtype = dtype
+        self.cdtype = cheb_dtype(dtype)
+        self.seg_numel = [int(n) for n in seg_numel]
+        lay = cheb_cache_layout(self.n_slots, self.cdtype, self.seg_numel)
+        self.seg_offset = [int(o) for o in lay["seg_offset"]]
+        self.slot_numel = int(lay["slot_numel"])
+        self.slot_stride_bytes = int(lay["slot_stride_bytes"])
+        self.arena_bytes = int(lay["arena_bytes"])
+        if arena is None:
+            device = torch.device("cuda", torch.cuda.current_device()) if device is None else device
+            arena = torch.empty(self.arena_bytes, dtype=torch.uint8, device=device)
+        _check_device_tensor(arena, "arena")
+        self.arena = arena
+        self.device = arena.device
+        self._h = cheb_cache_create(self.n_slots, self.cdtype, self.seg_numel,
+                                    arena.data_ptr(), arena.numel() * arena.element_size())
+
+    # -- lifetime ------------------------------------------------------------
+    def close(self):
+        if getattr(self, "_h", None) is not None:
+            cheb_cache_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    @property
+    def handle(self):
+        return self._h
+
+    # -- buffers -------------------------------------------------------------
+    def new_output(self) -> torch.Tensor:
+        return torch.empty(self.slot_numel, dtype=self.dtype, device=self.device)
+
+    def segment_views(self, flat: torch.Tensor, shapes=None) -> List[torch.Tensor]:
+        views = []
+        for s, (off, n) in enumerate(zip(self.seg_offset, self.seg_numel)):
+            v = flat[off:off + n]
+            views.append(v.view(shapes[s]) if shapes is not None else v)
+        return views
+
+    def _slot_tensor(self, addr: int) -> torch.Tensor:
+        start = addr - self.arena.data_ptr()
+        esz = torch.empty((), dtype=self.dtype).element_size()
+        raw = self.arena[start:start + self.slot_numel * esz]
+        return raw.view(self.dtype)
+
+    def entry(self, idx: int) -> torch.Tensor:
+        """Flat view of the held entry of age index idx (0 = oldest)."""
+        return self._slot_tensor(cheb_cache_entry(self._h, idx))
+
+    # -- the online stage ------------------------------------------------------
+    def push(self, t: float, segments: Sequence[torch.Tensor],
+             stream: Optional[torch.cuda.Stream] = None):
+        if len(segments) != len(self.seg_numel):
+            raise ChebError(_binding.CHEB_E_MISMATCH, "segment count differs from the layout")
+        for i, (s, n) in enumerate(zip(segments, self.seg_numel)):
+            _check_device_tensor(s, f"segments[{i}]")
+            if s.dtype != self.dtype or s.numel() != n:
+                raise ChebError(_binding.CHEB_E_MISMATCH, f"segments[{i}] differs from the layout")
+        cheb_cache_push(self._h, t, [s.data_ptr() for s in segments], _stream_handle(stream))
+
+    def begin_push(self) -> torch.Tensor:
+        """Flat view of the slot the next entry occupies (fused push)."""
+        return self._slot_tensor(cheb_cache_begin_push(self._h))
+
+    def commit(self, t: float):
+        cheb_cache_commit(self._h, t)
+
+    def reset(self):
+        cheb_cache_reset(self._h)
+
+    def history(self) -> np.ndarray:
+        return cheb_cache_history(self._h)
+
+    def _check_out(self, out: torch.Tensor):
+        _check_device_tensor(out, "out")
+        if out.dtype != self.dtype or out.numel() < self.slot_numel:
+            raise ChebError(_binding.CHEB_E_MISMATCH, "out differs from the slot layout")
+
+    def extrapolate(self, w, out: Optional[torch.Tensor] = None,
+                    stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+        out = self.new_output() if out is None else out
+        self._check_out(out)
+        cheb_extrapolate(self._h, w, out.data_ptr(), _stream_handle(stream))
+        return out
+
+    def extrapolate_at(self, target_t: float, out: Optional[torch.Tensor] = None,
+                       stream: Optional[torch.cuda.Stream] = None):
+        out = self.new_output() if out is None else out
+        self._check_out(out)
+        w = cheb_extrapolate_at(self._h, target_t, out.data_ptr(), _stream_handle(stream),
+                                n_slots=self.n_slots)
+        return out, w
+
+
+__all__ = [n for n in dir() if n.startswith("cheb_")] + [
+    "ChebCache", "ChebError", "combine", "precompute_weights", "CHEB_BF16", "CHEB_F32",
+    "CHEB_MAX_SLOTS", "CHEB_MAX_NODES", "LIB_PATH"]

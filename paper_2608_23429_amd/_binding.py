@@ -1,0 +1,232 @@
+"""ctypes binding of libcheb.so: the C entry points under their own names.
+
+Argument marshalling only.  Every step of the path runs in the library; there
+is no fallback: when libcheb.so is missing or does not load, importing the
+package fails.
+"""
+import ctypes
+import os
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libcheb.so")
+
+CHEB_OK = 0
+CHEB_E_INVAL = -1
+CHEB_E_DUPNODE = -2
+CHEB_E_NOTREADY = -3
+CHEB_E_DTYPE = -4
+CHEB_E_ALIGN = -5
+CHEB_E_HIP = -6
+CHEB_E_MISMATCH = -7
+CHEB_E_NONFINITE = -8
+
+CHEB_BF16 = 0
+CHEB_F32 = 1
+CHEB_MAX_SLOTS = 8
+CHEB_MAX_NODES = 64
+
+STATUS_NAMES = {
+    CHEB_E_INVAL: "CHEB_E_INVAL", CHEB_E_DUPNODE: "CHEB_E_DUPNODE",
+    CHEB_E_NOTREADY: "CHEB_E_NOTREADY", CHEB_E_DTYPE: "CHEB_E_DTYPE",
+    CHEB_E_ALIGN: "CHEB_E_ALIGN", CHEB_E_HIP: "CHEB_E_HIP",
+    CHEB_E_MISMATCH: "CHEB_E_MISMATCH", CHEB_E_NONFINITE: "CHEB_E_NONFINITE",
+}
+
+
+class ChebError(RuntimeError):
+    def __init__(self, code, message):
+        self.code = code
+        self.name = STATUS_NAMES.get(code, str(code))
+        super().__init__(f"{self.name}: {message}")
+
+
+class cheb_launch_config(ctypes.Structure):
+    _fields_ = [("unroll", ctypes.c_int32), ("nontemporal", ctypes.c_int32),
+                ("blocks_per_cu", ctypes.c_int32)]
+
+
+_dp = ctypes.POINTER(ctypes.c_double)
+_i64p = ctypes.POINTER(ctypes.c_int64)
+_i32p = ctypes.POINTER(ctypes.c_int32)
+_szp = ctypes.POINTER(ctypes.c_size_t)
+_vp = ctypes.c_void_p
+_vpp = ctypes.POINTER(ctypes.c_void_p)
+
+# name -> (argtypes)
+SIGNATURES = {
+    "cheb_last_error": [],
+    "cheb_version": [],
+    "cheb_precompute_weights": [_dp, ctypes.c_int32, _dp, ctypes.c_int32, _dp],
+    "cheb_combine": [_vpp, ctypes.c_int32, _dp, _vp, ctypes.c_int64, ctypes.c_int32, _vp],
+    "cheb_cache_layout": [ctypes.c_int32, ctypes.c_int32, _i64p, ctypes.c_int32, _i64p,
+                          _i64p, _szp, _szp],
+    "cheb_cache_create": [ctypes.POINTER(_vp), ctypes.c_int32, ctypes.c_int32, _i64p,
+                          ctypes.c_int32, _vp, ctypes.c_size_t],
+    "cheb_cache_destroy": [_vp],
+    "cheb_cache_reset": [_vp],
+    "cheb_cache_push": [_vp, ctypes.c_double, _vpp, _vp],
+    "cheb_cache_begin_push": [_vp, _vpp],
+    "cheb_cache_commit": [_vp, ctypes.c_double],
+    "cheb_cache_history": [_vp, _dp, _i32p],
+    "cheb_cache_entry": [_vp, ctypes.c_int32, _vpp],
+    "cheb_cache_segment_offset": [_vp, ctypes.c_int32, _i64p],
+    "cheb_cache_slot_numel": [_vp, _i64p],
+    "cheb_extrapolate": [_vp, _dp, _vp, _vp],
+    "cheb_extrapolate_at": [_vp, ctypes.c_double, _vp, _vp, _dp],
+    "cheb_get_launch_config": [ctypes.POINTER(cheb_launch_config)],
+    "cheb_set_launch_config": [ctypes.POINTER(cheb_launch_config)],
+}
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(
+            f"{LIB_PATH} is not built; run __graft_entry__.build() (hipcc, gfx950)")
+    lib = ctypes.CDLL(LIB_PATH)
+    for name, argtypes in SIGNATURES.items():
+        fn = getattr(lib, name)
+        fn.argtypes = argtypes
+        fn.restype = ctypes.c_char_p if name == "cheb_last_error" else ctypes.c_int
+    return lib
+
+
+LIB = _load()
+
+
+def _check(rc):
+    if rc != CHEB_OK:
+        raise ChebError(rc, LIB.cheb_last_error().decode(errors="replace"))
+    return rc
+
+
+def _f64(a):
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
+def _dptr(a):
+    return a.ctypes.data_as(_dp)
+
+
+def _voidp_array(ptrs):
+    return (ctypes.c_void_p * max(1, len(ptrs)))(*[ctypes.c_void_p(int(p)) for p in ptrs])
+
+
+def cheb_version() -> int:
+    return LIB.cheb_version()
+
+
+def cheb_last_error() -> str:
+    return LIB.cheb_last_error().decode(errors="replace")
+
+
+def cheb_precompute_weights(hist_t, target_t) -> np.ndarray:
+    """[n_target, n_hist] fp64 coefficient table (host)."""
+    h = _f64(hist_t).reshape(-1)
+    t = _f64(target_t).reshape(-1)
+    w = np.empty((t.size, h.size), dtype=np.float64)
+    _check(LIB.cheb_precompute_weights(_dptr(h), h.size, _dptr(t) if t.size else None,
+                                       t.size, _dptr(w) if w.size else None))
+    return w
+
+
+def cheb_combine(src_ptrs, w, out_ptr, numel, dtype, stream=0):
+    w = _f64(w).reshape(-1)
+    arr = _voidp_array(src_ptrs)
+    _check(LIB.cheb_combine(arr, len(src_ptrs), _dptr(w), ctypes.c_void_p(int(out_ptr)),
+                            int(numel), int(dtype), ctypes.c_void_p(int(stream))))
+
+
+def cheb_cache_layout(n_slots, dtype, seg_numel):
+    seg = np.ascontiguousarray(seg_numel, dtype=np.int64).reshape(-1)
+    off = np.empty_like(seg)
+    slot_numel = ctypes.c_int64()
+    stride = ctypes.c_size_t()
+    arena = ctypes.c_size_t()
+    _check(LIB.cheb_cache_layout(int(n_slots), int(dtype), seg.ctypes.data_as(_i64p), seg.size,
+                                 off.ctypes.data_as(_i64p), ctypes.byref(slot_numel),
+                                 ctypes.byref(stride), ctypes.byref(arena)))
+    return {"seg_offset": off, "slot_numel": slot_numel.value,
+            "slot_stride_bytes": stride.value, "arena_bytes": arena.value}
+
+
+def cheb_cache_create(n_slots, dtype, seg_numel, arena_ptr, arena_bytes):
+    seg = np.ascontiguousarray(seg_numel, dtype=np.int64).reshape(-1)
+    h = ctypes.c_void_p()
+    _check(LIB.cheb_cache_create(ctypes.byref(h), int(n_slots), int(dtype),
+                                 seg.ctypes.data_as(_i64p), seg.size,
+                                 ctypes.c_void_p(int(arena_ptr)), int(arena_bytes)))
+    return h
+
+
+def cheb_cache_destroy(handle):
+    _check(LIB.cheb_cache_destroy(handle))
+
+
+def cheb_cache_reset(handle):
+    _check(LIB.cheb_cache_reset(handle))
+
+
+def cheb_cache_push(handle, t, seg_ptrs, stream=0):
+    arr = _voidp_array(seg_ptrs)
+    _check(LIB.cheb_cache_push(handle, float(t), arr, ctypes.c_void_p(int(stream))))
+
+
+def cheb_cache_begin_push(handle) -> int:
+    p = ctypes.c_void_p()
+    _check(LIB.cheb_cache_begin_push(handle, ctypes.byref(p)))
+    return int(p.value or 0)
+
+
+def cheb_cache_commit(handle, t):
+    _check(LIB.cheb_cache_commit(handle, float(t)))
+
+
+def cheb_cache_history(handle, n_slots=CHEB_MAX_SLOTS):
+    t = np.empty(CHEB_MAX_SLOTS, dtype=np.float64)
+    n = ctypes.c_int32()
+    _check(LIB.cheb_cache_history(handle, _dptr(t), ctypes.byref(n)))
+    return t[:n.value].copy()
+
+
+def cheb_cache_entry(handle, idx) -> int:
+    p = ctypes.c_void_p()
+    _check(LIB.cheb_cache_entry(handle, int(idx), ctypes.byref(p)))
+    return int(p.value or 0)
+
+
+def cheb_cache_segment_offset(handle, seg) -> int:
+    o = ctypes.c_int64()
+    _check(LIB.cheb_cache_segment_offset(handle, int(seg), ctypes.byref(o)))
+    return o.value
+
+
+def cheb_cache_slot_numel(handle) -> int:
+    n = ctypes.c_int64()
+    _check(LIB.cheb_cache_slot_numel(handle, ctypes.byref(n)))
+    return n.value
+
+
+def cheb_extrapolate(handle, w, out_ptr, stream=0):
+    w = _f64(w).reshape(-1)
+    _check(LIB.cheb_extrapolate(handle, _dptr(w), ctypes.c_void_p(int(out_ptr)),
+                                ctypes.c_void_p(int(stream))))
+
+
+def cheb_extrapolate_at(handle, target_t, out_ptr, stream=0, n_slots=CHEB_MAX_SLOTS):
+    w = np.zeros(CHEB_MAX_SLOTS, dtype=np.float64)
+    _check(LIB.cheb_extrapolate_at(handle, float(target_t), ctypes.c_void_p(int(out_ptr)),
+                                   ctypes.c_void_p(int(stream)), _dptr(w)))
+    return w[:n_slots].copy()
+
+
+def cheb_get_launch_config():
+    c = cheb_launch_config()
+    _check(LIB.cheb_get_launch_config(ctypes.byref(c)))
+    return {"unroll": c.unroll, "nontemporal": c.nontemporal, "blocks_per_cu": c.blocks_per_cu}
+
+
+def cheb_set_launch_config(unroll=4, nontemporal=1, blocks_per_cu=0):
+    c = cheb_launch_config(int(unroll), int(nontemporal), int(blocks_per_cu))
+    _check(LIB.cheb_set_launch_config(ctypes.byref(c)))

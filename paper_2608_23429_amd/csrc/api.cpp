@@ -1,0 +1,199 @@
+// Host side of libcheb: error reporting, launch shape, weight
+// precomputation and the stateless combination entry point.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <mutex>
+
+#include "internal.h"
+
+namespace cheb {
+
+namespace {
+thread_local char g_error[512] = "";
+
+std::mutex g_shape_mutex;
+cheb_launch_config g_shape = {4, 1, 0};
+
+constexpr int kMaxDevices = 64;
+int g_cus[kMaxDevices] = {0};
+std::mutex g_cus_mutex;
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+}  // namespace
+
+int fail(int code, const char *fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_error, sizeof g_error, fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+int ok() {
+  g_error[0] = '\0';
+  return CHEB_OK;
+}
+
+cheb_launch_config launch_shape() {
+  std::lock_guard<std::mutex> lock(g_shape_mutex);
+  return g_shape;
+}
+
+int device_cus(int *cus) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(CHEB_E_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  if (dev >= 0 && dev < kMaxDevices) {
+    std::lock_guard<std::mutex> lock(g_cus_mutex);
+    if (g_cus[dev] > 0) {
+      *cus = g_cus[dev];
+      return CHEB_OK;
+    }
+  }
+  int n = 0;
+  e = hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess || n <= 0)
+    return fail(CHEB_E_HIP, "compute unit count: %s", hipGetErrorString(e));
+  if (dev >= 0 && dev < kMaxDevices) {
+    std::lock_guard<std::mutex> lock(g_cus_mutex);
+    g_cus[dev] = n;
+  }
+  *cus = n;
+  return CHEB_OK;
+}
+
+// Barycentric coefficients of one target (Section 3.2, coefficient
+// equation; Appendix A, rho_j = 1 / omega'(x_j) and the second form).
+// The abscissae are first mapped affinely so their span becomes [-1, 1]
+// (Section 3.3); Lagrange coefficients are unchanged by any affine map, and
+// the map keeps the products in omega' near unit scale.
+int weights_row(const double *x, int n, double target, double *w) {
+  if (n < 1 || n > CHEB_MAX_NODES)
+    return fail(CHEB_E_INVAL, "history size %d outside 1..%d", n, CHEB_MAX_NODES);
+  if (!isfinite(target)) return fail(CHEB_E_NONFINITE, "target abscissa is not finite");
+  double lo = x[0], hi = x[0];
+  for (int j = 0; j < n; ++j) {
+    if (!isfinite(x[j])) return fail(CHEB_E_NONFINITE, "history abscissa %d is not finite", j);
+    lo = fmin(lo, x[j]);
+    hi = fmax(hi, x[j]);
+  }
+  for (int j = 0; j < n; ++j)
+    for (int k = 0; k < j; ++k)
+      if (x[j] == x[k])
+        return fail(CHEB_E_DUPNODE, "history abscissae %d and %d are equal (%.17g)", k, j, x[j]);
+  // Target on a node: the interpolant takes the node's value.
+  for (int j = 0; j < n; ++j) {
+    if (target == x[j]) {
+      for (int k = 0; k < n; ++k) w[k] = (k == j) ? 1.0 : 0.0;
+      return CHEB_OK;
+    }
+  }
+  if (n == 1) {
+    w[0] = 1.0;
+    return CHEB_OK;
+  }
+  const double mid = 0.5 * (lo + hi);
+  const double inv_half = 2.0 / (hi - lo);
+  double y[CHEB_MAX_NODES];
+  for (int j = 0; j < n; ++j) y[j] = (x[j] - mid) * inv_half;
+  const double yt = (target - mid) * inv_half;
+  double terms[CHEB_MAX_NODES];
+  double total = 0.0;
+  for (int j = 0; j < n; ++j) {
+    double omega_prime = 1.0;
+    for (int k = 0; k < n; ++k)
+      if (k != j) omega_prime *= y[j] - y[k];
+    const double gap = yt - y[j];
+    if (gap == 0.0) {  // distinct abscissae that the map rounded together
+      for (int k = 0; k < n; ++k) w[k] = (k == j) ? 1.0 : 0.0;
+      return CHEB_OK;
+    }
+    terms[j] = 1.0 / (omega_prime * gap);
+    total += terms[j];
+  }
+  for (int j = 0; j < n; ++j) w[j] = terms[j] / total;
+  return CHEB_OK;
+}
+
+}  // namespace cheb
+
+using namespace cheb;
+
+extern "C" {
+
+const char *cheb_last_error(void) { return g_error; }
+
+int cheb_version(void) { return CHEB_VERSION; }
+
+int cheb_get_launch_config(cheb_launch_config *cfg) {
+  if (!cfg) return fail(CHEB_E_INVAL, "cfg is NULL");
+  *cfg = launch_shape();
+  return ok();
+}
+
+int cheb_set_launch_config(const cheb_launch_config *cfg) {
+  if (!cfg) return fail(CHEB_E_INVAL, "cfg is NULL");
+  if (cfg->unroll != 1 && cfg->unroll != 2 && cfg->unroll != 4)
+    return fail(CHEB_E_INVAL, "unroll must be 1, 2 or 4 (got %d)", cfg->unroll);
+  if (cfg->nontemporal != 0 && cfg->nontemporal != 1)
+    return fail(CHEB_E_INVAL, "nontemporal must be 0 or 1 (got %d)", cfg->nontemporal);
+  if (cfg->blocks_per_cu < 0 || cfg->blocks_per_cu > 64)
+    return fail(CHEB_E_INVAL, "blocks_per_cu must be 0..64 (got %d)", cfg->blocks_per_cu);
+  std::lock_guard<std::mutex> lock(g_shape_mutex);
+  g_shape = *cfg;
+  return ok();
+}
+
+int cheb_precompute_weights(const double *hist_t, int32_t n_hist, const double *target_t,
+                            int32_t n_target, double *w_out) {
+  if (!hist_t) return fail(CHEB_E_INVAL, "hist_t is NULL");
+  if (n_target < 0) return fail(CHEB_E_INVAL, "n_target is negative");
+  if (n_target > 0 && (!target_t || !w_out)) return fail(CHEB_E_INVAL, "target_t or w_out is NULL");
+  if (n_hist < 1 || n_hist > CHEB_MAX_NODES)
+    return fail(CHEB_E_INVAL, "n_hist %d outside 1..%d", n_hist, CHEB_MAX_NODES);
+  // Validate every row before writing any, so w_out is untouched on error.
+  double row[CHEB_MAX_NODES];
+  for (int32_t m = 0; m < n_target; ++m) {
+    int rc = weights_row(hist_t, n_hist, target_t[m], row);
+    if (rc != CHEB_OK) return rc;
+  }
+  if (n_target == 0) {
+    int rc = weights_row(hist_t, n_hist, hist_t[0], row);  // node checks only
+    if (rc != CHEB_OK) return rc;
+  }
+  for (int32_t m = 0; m < n_target; ++m) {
+    weights_row(hist_t, n_hist, target_t[m], row);
+    memcpy(w_out + size_t(m) * n_hist, row, sizeof(double) * n_hist);
+  }
+  return ok();
+}
+
+int cheb_combine(const void *const *src, int32_t n_src, const double *w, void *out,
+                 int64_t numel, int32_t dtype, void *stream) {
+  if (!valid_dtype(dtype)) return fail(CHEB_E_DTYPE, "unknown dtype %d", dtype);
+  if (n_src < 1 || n_src > CHEB_MAX_SLOTS)
+    return fail(CHEB_E_INVAL, "n_src %d outside 1..%d", n_src, CHEB_MAX_SLOTS);
+  if (!src || !w) return fail(CHEB_E_INVAL, "src or w is NULL");
+  if (numel < 0) return fail(CHEB_E_INVAL, "numel is negative");
+  if (numel / elems_per_vec(dtype) >= kMaxVecs)
+    return fail(CHEB_E_INVAL, "numel %lld too large for one launch", (long long)numel);
+  if (numel == 0) return ok();
+  if (!out) return fail(CHEB_E_INVAL, "out is NULL");
+  if (!aligned16(out)) return fail(CHEB_E_ALIGN, "out is not 16-byte aligned");
+  const uintptr_t bytes = uintptr_t(numel) * elem_bytes(dtype);
+  const uintptr_t o0 = reinterpret_cast<uintptr_t>(out);
+  for (int k = 0; k < n_src; ++k) {
+    if (!src[k]) return fail(CHEB_E_INVAL, "src[%d] is NULL", k);
+    if (!aligned16(src[k])) return fail(CHEB_E_ALIGN, "src[%d] is not 16-byte aligned", k);
+    if (!isfinite(w[k])) return fail(CHEB_E_NONFINITE, "w[%d] is not finite", k);
+    const uintptr_t s0 = reinterpret_cast<uintptr_t>(src[k]);
+    if (s0 < o0 + bytes && o0 < s0 + bytes)
+      return fail(CHEB_E_INVAL, "out overlaps src[%d]", k);
+  }
+  return launch_combine(dtype, src, n_src, w, out, numel, static_cast<hipStream_t>(stream));
+}
+
+}  // extern "C"

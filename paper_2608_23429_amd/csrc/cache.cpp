@@ -1,0 +1,259 @@
+// History cache: the fixed-size FIFO of full-step features (paper,
+// Section 3.3, forward application; Algorithm 1, online stage) kept as a
+// ring of slots in one caller-owned device arena.
+#include <math.h>
+#include <string.h>
+
+#include <new>
+#include <vector>
+
+#include "internal.h"
+
+using namespace cheb;
+
+struct cheb_cache {
+  int32_t n_slots = 0;
+  int32_t dtype = CHEB_BF16;
+  std::vector<int64_t> seg_numel;
+  std::vector<int64_t> seg_offset;
+  int64_t slot_numel = 0;
+  size_t slot_stride = 0;
+  char *arena = nullptr;
+  size_t arena_bytes = 0;
+  // Ring state: `head` is the slot the next entry goes to; the `count` held
+  // entries, oldest first, are in slots head - count, ..., head - 1 (mod n).
+  double slot_t[CHEB_MAX_SLOTS] = {0};
+  int32_t head = 0;
+  int32_t count = 0;
+  bool push_open = false;
+
+  int32_t slot_of_age(int32_t age) const {
+    return ((head - count + age) % n_slots + n_slots) % n_slots;
+  }
+  char *slot_ptr(int32_t slot) const { return arena + size_t(slot) * slot_stride; }
+};
+
+namespace {
+
+constexpr size_t kSlotAlign = 256;
+
+int layout(int32_t n_slots, int32_t dtype, const int64_t *seg_numel, int32_t n_segs,
+           std::vector<int64_t> *offsets, int64_t *slot_numel, size_t *stride,
+           size_t *arena_bytes) {
+  if (!valid_dtype(dtype)) return fail(CHEB_E_DTYPE, "unknown dtype %d", dtype);
+  if (n_slots < 1 || n_slots > CHEB_MAX_SLOTS)
+    return fail(CHEB_E_INVAL, "n_slots %d outside 1..%d", n_slots, CHEB_MAX_SLOTS);
+  if (n_segs < 1) return fail(CHEB_E_INVAL, "n_segs must be at least 1");
+  if (!seg_numel) return fail(CHEB_E_INVAL, "seg_numel is NULL");
+  const int64_t vec = elems_per_vec(dtype);
+  offsets->assign(size_t(n_segs), 0);
+  int64_t pos = 0;
+  for (int32_t s = 0; s < n_segs; ++s) {
+    if (seg_numel[s] < 0) return fail(CHEB_E_INVAL, "seg_numel[%d] is negative", s);
+    (*offsets)[size_t(s)] = pos;
+    pos += (seg_numel[s] + vec - 1) / vec * vec;
+    if (pos / vec >= kMaxVecs) return fail(CHEB_E_INVAL, "cache slot too large");
+  }
+  const size_t bytes = size_t(pos) * size_t(elem_bytes(dtype));
+  const size_t str = (bytes + kSlotAlign - 1) / kSlotAlign * kSlotAlign;
+  *slot_numel = pos;
+  *stride = str;
+  *arena_bytes = str * size_t(n_slots);
+  return CHEB_OK;
+}
+
+bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// CHEB_E_DUPNODE when t equals an abscissa that stays held after the next
+// entry goes in (a full ring drops its oldest first).
+int check_new_abscissa(const cheb_cache *c, double t) {
+  if (!isfinite(t)) return fail(CHEB_E_NONFINITE, "abscissa is not finite");
+  const int32_t first = (c->count == c->n_slots) ? 1 : 0;
+  for (int32_t a = first; a < c->count; ++a)
+    if (c->slot_t[c->slot_of_age(a)] == t)
+      return fail(CHEB_E_DUPNODE, "abscissa %.17g is already held", t);
+  return CHEB_OK;
+}
+
+// Claims the slot for the next entry, dropping the oldest entry if full.
+int32_t claim_slot(cheb_cache *c) {
+  if (c->count == c->n_slots) c->count -= 1;  // the oldest lives in slot `head`
+  return c->head;
+}
+
+void record(cheb_cache *c, double t) {
+  c->slot_t[c->head] = t;
+  c->head = (c->head + 1) % c->n_slots;
+  c->count += 1;
+}
+
+}  // namespace
+
+extern "C" {
+
+int cheb_cache_layout(int32_t n_slots, int32_t dtype, const int64_t *seg_numel, int32_t n_segs,
+                      int64_t *seg_offset, int64_t *slot_numel, size_t *slot_stride_bytes,
+                      size_t *arena_bytes) {
+  std::vector<int64_t> off;
+  int64_t sn = 0;
+  size_t st = 0, ab = 0;
+  int rc = layout(n_slots, dtype, seg_numel, n_segs, &off, &sn, &st, &ab);
+  if (rc != CHEB_OK) return rc;
+  if (seg_offset) memcpy(seg_offset, off.data(), sizeof(int64_t) * off.size());
+  if (slot_numel) *slot_numel = sn;
+  if (slot_stride_bytes) *slot_stride_bytes = st;
+  if (arena_bytes) *arena_bytes = ab;
+  return ok();
+}
+
+int cheb_cache_create(cheb_cache **out, int32_t n_slots, int32_t dtype, const int64_t *seg_numel,
+                      int32_t n_segs, void *arena, size_t arena_bytes) {
+  if (!out) return fail(CHEB_E_INVAL, "out is NULL");
+  *out = nullptr;
+  std::vector<int64_t> off;
+  int64_t sn = 0;
+  size_t st = 0, need = 0;
+  int rc = layout(n_slots, dtype, seg_numel, n_segs, &off, &sn, &st, &need);
+  if (rc != CHEB_OK) return rc;
+  if (!arena) return fail(CHEB_E_INVAL, "arena is NULL");
+  if (!aligned(arena, kSlotAlign)) return fail(CHEB_E_ALIGN, "arena is not 256-byte aligned");
+  if (arena_bytes < need)
+    return fail(CHEB_E_MISMATCH, "arena holds %zu bytes, the layout needs %zu", arena_bytes, need);
+  cheb_cache *c = new (std::nothrow) cheb_cache();
+  if (!c) return fail(CHEB_E_INVAL, "out of host memory");
+  c->n_slots = n_slots;
+  c->dtype = dtype;
+  c->seg_numel.assign(seg_numel, seg_numel + n_segs);
+  c->seg_offset = std::move(off);
+  c->slot_numel = sn;
+  c->slot_stride = st;
+  c->arena = static_cast<char *>(arena);
+  c->arena_bytes = arena_bytes;
+  *out = c;
+  return ok();
+}
+
+int cheb_cache_destroy(cheb_cache *c) {
+  delete c;
+  return ok();
+}
+
+int cheb_cache_reset(cheb_cache *c) {
+  if (!c) return fail(CHEB_E_INVAL, "cache is NULL");
+  c->head = 0;
+  c->count = 0;
+  c->push_open = false;
+  return ok();
+}
+
+int cheb_cache_push(cheb_cache *c, double t, const void *const *seg_src, void *stream) {
+  if (!c) return fail(CHEB_E_INVAL, "cache is NULL");
+  if (c->push_open) return fail(CHEB_E_NOTREADY, "a fused push is open");
+  if (!seg_src) return fail(CHEB_E_INVAL, "seg_src is NULL");
+  int rc = check_new_abscissa(c, t);
+  if (rc != CHEB_OK) return rc;
+  const size_t n_segs = c->seg_numel.size();
+  std::vector<GatherSeg> segs(n_segs);
+  for (size_t s = 0; s < n_segs; ++s) {
+    if (c->seg_numel[s] > 0) {
+      if (!seg_src[s]) return fail(CHEB_E_INVAL, "seg_src[%zu] is NULL", s);
+      if (!aligned(seg_src[s], 16))
+        return fail(CHEB_E_ALIGN, "seg_src[%zu] is not 16-byte aligned", s);
+    }
+    segs[s] = GatherSeg{seg_src[s], c->seg_offset[s], c->seg_numel[s]};
+  }
+  // The slot receiving the entry is the oldest one when the ring is full.
+  const int32_t slot = (c->count == c->n_slots) ? c->slot_of_age(0) : c->head;
+  rc = launch_gather(c->dtype, c->slot_ptr(slot), segs.data(), int(n_segs),
+                     static_cast<hipStream_t>(stream));
+  if (rc != CHEB_OK) return rc;
+  claim_slot(c);
+  record(c, t);
+  return ok();
+}
+
+int cheb_cache_begin_push(cheb_cache *c, void **slot_base) {
+  if (!c || !slot_base) return fail(CHEB_E_INVAL, "cache or slot_base is NULL");
+  if (c->push_open) return fail(CHEB_E_NOTREADY, "a fused push is already open");
+  const int32_t slot = claim_slot(c);
+  c->push_open = true;
+  *slot_base = c->slot_ptr(slot);
+  return ok();
+}
+
+int cheb_cache_commit(cheb_cache *c, double t) {
+  if (!c) return fail(CHEB_E_INVAL, "cache is NULL");
+  if (!c->push_open) return fail(CHEB_E_NOTREADY, "no fused push is open");
+  if (!isfinite(t)) return fail(CHEB_E_NONFINITE, "abscissa is not finite");
+  for (int32_t a = 0; a < c->count; ++a)
+    if (c->slot_t[c->slot_of_age(a)] == t)
+      return fail(CHEB_E_DUPNODE, "abscissa %.17g is already held", t);
+  record(c, t);
+  c->push_open = false;
+  return ok();
+}
+
+int cheb_cache_history(const cheb_cache *c, double *t_out, int32_t *count) {
+  if (!c || !count) return fail(CHEB_E_INVAL, "cache or count is NULL");
+  *count = c->count;
+  if (t_out)
+    for (int32_t a = 0; a < c->count; ++a) t_out[a] = c->slot_t[c->slot_of_age(a)];
+  return ok();
+}
+
+int cheb_cache_entry(const cheb_cache *c, int32_t idx, void **slot_base) {
+  if (!c || !slot_base) return fail(CHEB_E_INVAL, "cache or slot_base is NULL");
+  if (idx < 0 || idx >= c->count)
+    return fail(CHEB_E_INVAL, "entry %d outside 0..%d", idx, c->count - 1);
+  *slot_base = c->slot_ptr(c->slot_of_age(idx));
+  return ok();
+}
+
+int cheb_cache_segment_offset(const cheb_cache *c, int32_t seg, int64_t *elem_offset) {
+  if (!c || !elem_offset) return fail(CHEB_E_INVAL, "cache or elem_offset is NULL");
+  if (seg < 0 || size_t(seg) >= c->seg_offset.size())
+    return fail(CHEB_E_INVAL, "segment %d out of range", seg);
+  *elem_offset = c->seg_offset[size_t(seg)];
+  return ok();
+}
+
+int cheb_cache_slot_numel(const cheb_cache *c, int64_t *numel) {
+  if (!c || !numel) return fail(CHEB_E_INVAL, "cache or numel is NULL");
+  *numel = c->slot_numel;
+  return ok();
+}
+
+int cheb_extrapolate(cheb_cache *c, const double *w, void *out, void *stream) {
+  if (!c || !w) return fail(CHEB_E_INVAL, "cache or w is NULL");
+  if (c->push_open) return fail(CHEB_E_NOTREADY, "a fused push is open");
+  if (c->count < c->n_slots)
+    return fail(CHEB_E_NOTREADY, "history holds %d of %d entries", c->count, c->n_slots);
+  const void *src[CHEB_MAX_SLOTS];
+  for (int32_t a = 0; a < c->n_slots; ++a) src[a] = c->slot_ptr(c->slot_of_age(a));
+  if (c->slot_numel > 0) {
+    if (!out) return fail(CHEB_E_INVAL, "out is NULL");
+    const uintptr_t o0 = reinterpret_cast<uintptr_t>(out);
+    const uintptr_t a0 = reinterpret_cast<uintptr_t>(c->arena);
+    const uintptr_t ob = uintptr_t(c->slot_numel) * uintptr_t(elem_bytes(c->dtype));
+    if (o0 < a0 + c->arena_bytes && a0 < o0 + ob)
+      return fail(CHEB_E_INVAL, "out overlaps the cache arena");
+  }
+  return cheb_combine(src, c->n_slots, w, out, c->slot_numel, c->dtype, stream);
+}
+
+int cheb_extrapolate_at(cheb_cache *c, double target_t, void *out, void *stream,
+                        double *w_used) {
+  if (!c) return fail(CHEB_E_INVAL, "cache is NULL");
+  if (c->push_open) return fail(CHEB_E_NOTREADY, "a fused push is open");
+  if (c->count < c->n_slots)
+    return fail(CHEB_E_NOTREADY, "history holds %d of %d entries", c->count, c->n_slots);
+  double t[CHEB_MAX_SLOTS], w[CHEB_MAX_SLOTS];
+  for (int32_t a = 0; a < c->n_slots; ++a) t[a] = c->slot_t[c->slot_of_age(a)];
+  int rc = weights_row(t, c->n_slots, target_t, w);
+  if (rc != CHEB_OK) return rc;
+  rc = cheb_extrapolate(c, w, out, stream);
+  if (rc == CHEB_OK && w_used) memcpy(w_used, w, sizeof(double) * size_t(c->n_slots));
+  return rc;
+}
+
+}  // extern "C"

@@ -1,0 +1,53 @@
+// Internal declarations shared by the host sources and the kernel launchers
+// of libcheb.  Not installed; the public interface is include/cheb.h.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#include "cheb.h"
+
+namespace cheb {
+
+// Records a message for cheb_last_error() and returns `code`.
+int fail(int code, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
+// Clears the thread's message and returns CHEB_OK.
+int ok();
+
+// Storage type traits.
+inline int elem_bytes(int dtype) { return dtype == CHEB_BF16 ? 2 : 4; }
+inline int elems_per_vec(int dtype) { return 16 / elem_bytes(dtype); }
+inline bool valid_dtype(int dtype) { return dtype == CHEB_BF16 || dtype == CHEB_F32; }
+
+// Largest number of 16-byte vectors one streaming launch covers (keeps every
+// in-kernel index below 2^31 so 32-bit index arithmetic cannot wrap).
+constexpr int64_t kMaxVecs = int64_t(1) << 31;
+
+// Current process-wide launch shape.
+cheb_launch_config launch_shape();
+
+// Number of compute units of the current device (cached per device).
+int device_cus(int *cus);
+
+// One row of barycentric interpolation coefficients (host, fp64).  Returns
+// CHEB_OK or an error code with the message set.
+int weights_row(const double *x, int n, double target, double *w);
+
+// out[i] = sum_k w[k] * src[k][i], i < numel.  Arguments already validated:
+// 1 <= n <= CHEB_MAX_SLOTS, pointers 16-byte aligned, numel below the limit.
+int launch_combine(int dtype, const void *const *src, int n, const double *w,
+                   void *out, int64_t numel, hipStream_t stream);
+
+// Segment copy into one slot; zero-fills each segment's padding up to the
+// next 16-byte boundary.
+struct GatherSeg {
+  const void *src;     // device, 16-byte aligned
+  int64_t dst_offset;  // elements from the slot base (16-byte multiple)
+  int64_t numel;       // elements to copy
+};
+int launch_gather(int dtype, void *slot_base, const GatherSeg *segs, int n_segs,
+                  hipStream_t stream);
+
+}  // namespace cheb

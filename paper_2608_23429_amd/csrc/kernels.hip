@@ -1,0 +1,342 @@
+// Device kernels of libcheb for gfx950 (CDNA4, wave64).
+//
+// 1. The skipped-step prediction (paper, Section 3.3, forward application
+//    equation; Algorithm 1, extrapolation branch): out = sum_k w_k H_k over
+//    the flattened feature cache.  Pure streaming work: (n+1) x 16 bytes of
+//    HBM traffic per 16-byte output vector and 2n flops per element, far
+//    below the fp32 ridge point, so the kernel is laid out for bandwidth:
+//    128-bit coalesced loads (a wave covers 1 KiB contiguous per load
+//    instruction), all n x unroll loads of a thread issued before any
+//    arithmetic, weights as kernel arguments (they live in SGPRs), fp32
+//    accumulation for bf16 storage and fp64 for fp32 storage, and one
+//    hardware round-to-nearest-even pack per element pair
+//    (v_cvt_pk_bf16_f32).  No LDS: nothing is reused across lanes.
+// 2. The full-step push (Algorithm 1, full computation: store (s, f_s) in
+//    the history): one launch copies up to 64 segments into a slot.
+#include <hip/hip_runtime.h>
+
+#include <stdint.h>
+#include <string.h>
+
+#include <algorithm>
+
+#include "internal.h"
+
+namespace cheb {
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kBlock = 256;  // 4 waves of 64 lanes
+
+template <bool NT>
+__device__ __forceinline__ u32x4 load16(const u32x4 *p) {
+  if constexpr (NT) return __builtin_nontemporal_load(p);
+  else return *p;
+}
+
+template <bool NT>
+__device__ __forceinline__ void store16(u32x4 *p, u32x4 v) {
+  if constexpr (NT) __builtin_nontemporal_store(v, p);
+  else *p = v;
+}
+
+// History pointers (oldest to newest) and weights, passed by value as kernel
+// arguments.
+template <int NS, typename W>
+struct Hist {
+  const u32x4 *p[NS];
+  W w[NS];
+};
+
+// Ragged end of a stateless combination: `count` (< elements per vector)
+// trailing elements starting at element `first`, done by block 0.
+struct Tail {
+  uint32_t count;
+  uint64_t first;
+};
+
+// ---- bfloat16 storage, fp32 accumulation ---------------------------------
+
+struct Bf16Op {
+  using W = float;
+  using E = uint16_t;
+
+  __device__ __forceinline__ static float lo(uint32_t word) {
+    return __uint_as_float(word << 16);  // element 2q (low half)
+  }
+  __device__ __forceinline__ static float hi(uint32_t word) {
+    return __uint_as_float(word & 0xffff0000u);  // element 2q+1
+  }
+
+  template <int NS>
+  __device__ __forceinline__ static u32x4 vec(const u32x4 (&v)[NS], const W (&w)[NS]) {
+    float a[8];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      a[2 * q] = w[0] * lo(v[0][q]);
+      a[2 * q + 1] = w[0] * hi(v[0][q]);
+    }
+#pragma unroll
+    for (int k = 1; k < NS; ++k) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        a[2 * q] = fmaf(w[k], lo(v[k][q]), a[2 * q]);
+        a[2 * q + 1] = fmaf(w[k], hi(v[k][q]), a[2 * q + 1]);
+      }
+    }
+    u32x4 r;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      f32x2 pair = {a[2 * q], a[2 * q + 1]};
+      r[q] = __builtin_bit_cast(uint32_t, __builtin_convertvector(pair, bf16x2));
+    }
+    return r;
+  }
+
+  template <int NS>
+  __device__ __forceinline__ static E scalar(const E *const (&p)[NS], const W (&w)[NS],
+                                             uint64_t i) {
+    float a = w[0] * __uint_as_float(uint32_t(p[0][i]) << 16);
+#pragma unroll
+    for (int k = 1; k < NS; ++k) a = fmaf(w[k], __uint_as_float(uint32_t(p[k][i]) << 16), a);
+    return __builtin_bit_cast(uint16_t, static_cast<__bf16>(a));
+  }
+};
+
+// ---- binary32 storage, fp64 accumulation ---------------------------------
+
+struct F32Op {
+  using W = double;
+  using E = float;
+
+  template <int NS>
+  __device__ __forceinline__ static u32x4 vec(const u32x4 (&v)[NS], const W (&w)[NS]) {
+    double a[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) a[q] = w[0] * double(__uint_as_float(v[0][q]));
+#pragma unroll
+    for (int k = 1; k < NS; ++k)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) a[q] = fma(w[k], double(__uint_as_float(v[k][q])), a[q]);
+    u32x4 r;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) r[q] = __float_as_uint(float(a[q]));
+    return r;
+  }
+
+  template <int NS>
+  __device__ __forceinline__ static E scalar(const E *const (&p)[NS], const W (&w)[NS],
+                                             uint64_t i) {
+    double a = w[0] * double(p[0][i]);
+#pragma unroll
+    for (int k = 1; k < NS; ++k) a = fma(w[k], double(p[k][i]), a);
+    return float(a);
+  }
+};
+
+// ---- the streaming kernel -------------------------------------------------
+//
+// The vector range [0, n_vec) is cut into tiles of kBlock * U vectors.  A
+// block takes tiles blockIdx.x, blockIdx.x + gridDim.x, ... (one tile per
+// block when the grid covers the range, a persistent loop otherwise).  In a
+// tile, lane t of the block handles vectors t, t + kBlock, ..., so every
+// load instruction of a wave reads 64 consecutive 16-byte vectors.
+template <class Op, int NS, int U, bool NT>
+__global__ __launch_bounds__(kBlock) void combine_kernel(Hist<NS, typename Op::W> h,
+                                                         u32x4 *__restrict__ out,
+                                                         uint32_t n_vec, uint32_t n_tiles,
+                                                         Tail tail) {
+  for (uint32_t tile = blockIdx.x; tile < n_tiles; tile += gridDim.x) {
+    const uint32_t base = tile * uint32_t(kBlock * U) + threadIdx.x;
+    if (base + uint32_t((U - 1) * kBlock) < n_vec) {
+      u32x4 v[U][NS];
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int k = 0; k < NS; ++k) v[u][k] = load16<NT>(h.p[k] + base + u * kBlock);
+#pragma unroll
+      for (int u = 0; u < U; ++u) store16<NT>(out + base + u * kBlock, Op::template vec<NS>(v[u], h.w));
+    } else {
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const uint32_t i = base + u * kBlock;
+        if (i < n_vec) {
+          u32x4 v[NS];
+#pragma unroll
+          for (int k = 0; k < NS; ++k) v[k] = load16<NT>(h.p[k] + i);
+          store16<NT>(out + i, Op::template vec<NS>(v, h.w));
+        }
+      }
+    }
+  }
+  if (tail.count != 0 && blockIdx.x == 0 && threadIdx.x < tail.count) {
+    using E = typename Op::E;
+    const E *p[NS];
+#pragma unroll
+    for (int k = 0; k < NS; ++k) p[k] = reinterpret_cast<const E *>(h.p[k]);
+    const uint64_t i = tail.first + threadIdx.x;
+    reinterpret_cast<E *>(out)[i] = Op::template scalar<NS>(p, h.w, i);
+  }
+}
+
+template <class Op, int NS, int U, bool NT>
+hipError_t launch_shape_ns(const Hist<NS, typename Op::W> &h, u32x4 *out, uint32_t n_vec,
+                           Tail tail, int blocks_per_cu, int cus, hipStream_t s) {
+  const uint32_t per_tile = uint32_t(kBlock * U);
+  const uint32_t n_tiles = (n_vec + per_tile - 1) / per_tile;
+  uint32_t grid = std::max<uint32_t>(n_tiles, 1u);
+  if (blocks_per_cu > 0) grid = std::min<uint32_t>(grid, uint32_t(blocks_per_cu) * uint32_t(cus));
+  hipLaunchKernelGGL((combine_kernel<Op, NS, U, NT>), dim3(grid), dim3(kBlock), 0, s, h, out,
+                     n_vec, n_tiles, tail);
+  return hipGetLastError();
+}
+
+template <class Op, int NS>
+hipError_t launch_ns(const void *const *src, const double *w, void *out, int64_t numel,
+                     const cheb_launch_config &cfg, int cus, hipStream_t s) {
+  constexpr int kVec = 16 / int(sizeof(typename Op::E));
+  Hist<NS, typename Op::W> h;
+  for (int k = 0; k < NS; ++k) {
+    h.p[k] = static_cast<const u32x4 *>(src[k]);
+    h.w[k] = static_cast<typename Op::W>(w[k]);
+  }
+  const uint32_t n_vec = uint32_t(numel / kVec);
+  Tail tail{uint32_t(numel % kVec), uint64_t(numel / kVec) * kVec};
+  u32x4 *o = static_cast<u32x4 *>(out);
+  const bool nt = cfg.nontemporal != 0;
+  switch (cfg.unroll) {
+    case 1:
+      return nt ? launch_shape_ns<Op, NS, 1, true>(h, o, n_vec, tail, cfg.blocks_per_cu, cus, s)
+                : launch_shape_ns<Op, NS, 1, false>(h, o, n_vec, tail, cfg.blocks_per_cu, cus, s);
+    case 2:
+      return nt ? launch_shape_ns<Op, NS, 2, true>(h, o, n_vec, tail, cfg.blocks_per_cu, cus, s)
+                : launch_shape_ns<Op, NS, 2, false>(h, o, n_vec, tail, cfg.blocks_per_cu, cus, s);
+    default:
+      return nt ? launch_shape_ns<Op, NS, 4, true>(h, o, n_vec, tail, cfg.blocks_per_cu, cus, s)
+                : launch_shape_ns<Op, NS, 4, false>(h, o, n_vec, tail, cfg.blocks_per_cu, cus, s);
+  }
+}
+
+template <class Op>
+hipError_t launch_op(const void *const *src, int n, const double *w, void *out, int64_t numel,
+                     const cheb_launch_config &cfg, int cus, hipStream_t s) {
+  switch (n) {
+    case 1: return launch_ns<Op, 1>(src, w, out, numel, cfg, cus, s);
+    case 2: return launch_ns<Op, 2>(src, w, out, numel, cfg, cus, s);
+    case 3: return launch_ns<Op, 3>(src, w, out, numel, cfg, cus, s);
+    case 4: return launch_ns<Op, 4>(src, w, out, numel, cfg, cus, s);
+    case 5: return launch_ns<Op, 5>(src, w, out, numel, cfg, cus, s);
+    case 6: return launch_ns<Op, 6>(src, w, out, numel, cfg, cus, s);
+    case 7: return launch_ns<Op, 7>(src, w, out, numel, cfg, cus, s);
+    default: return launch_ns<Op, 8>(src, w, out, numel, cfg, cus, s);
+  }
+}
+
+// ---- full-step push: segment gather into one slot --------------------------
+
+constexpr int kGatherMax = 64;
+constexpr int kGatherUnroll = 4;
+constexpr uint32_t kGatherChunk = kBlock * kGatherUnroll;  // vectors per block
+
+struct GatherArgs {
+  const void *src[kGatherMax];
+  uint64_t dst_offset[kGatherMax];  // elements
+  uint64_t numel[kGatherMax];
+  uint32_t chunk_begin[kGatherMax + 1];  // prefix sums of blocks per segment
+  int32_t n;
+};
+
+template <typename E>
+__global__ __launch_bounds__(kBlock) void gather_kernel(GatherArgs a, char *__restrict__ slot) {
+  constexpr int kVec = 16 / int(sizeof(E));
+  // Segment of this block: the last s with chunk_begin[s] <= blockIdx.x.
+  int s = 0;
+  while (s + 1 < a.n && a.chunk_begin[s + 1] <= blockIdx.x) ++s;
+  const uint32_t chunk = blockIdx.x - a.chunk_begin[s];
+  const uint64_t numel = a.numel[s];
+  const uint64_t n_full = numel / kVec;
+  const uint32_t rem = uint32_t(numel % kVec);
+  const u32x4 *src = static_cast<const u32x4 *>(a.src[s]);
+  E *dst_e = reinterpret_cast<E *>(slot) + a.dst_offset[s];
+  u32x4 *dst = reinterpret_cast<u32x4 *>(dst_e);
+  const uint64_t base = uint64_t(chunk) * kGatherChunk + threadIdx.x;
+  u32x4 v[kGatherUnroll];
+#pragma unroll
+  for (int u = 0; u < kGatherUnroll; ++u) {
+    const uint64_t i = base + u * kBlock;
+    if (i < n_full) v[u] = src[i];
+  }
+#pragma unroll
+  for (int u = 0; u < kGatherUnroll; ++u) {
+    const uint64_t i = base + u * kBlock;
+    if (i < n_full) {
+      dst[i] = v[u];
+    } else if (i == n_full && rem != 0) {
+      // Last, partial vector: copy the remaining elements one by one and
+      // zero the padding up to the 16-byte boundary.
+      const E *src_e = static_cast<const E *>(a.src[s]);
+      E tmp[kVec];
+#pragma unroll
+      for (int e = 0; e < kVec; ++e) tmp[e] = (uint32_t(e) < rem) ? src_e[n_full * kVec + e] : E(0);
+      u32x4 packed;
+      memcpy(&packed, tmp, 16);
+      dst[i] = packed;
+    }
+  }
+}
+
+}  // namespace
+
+int launch_combine(int dtype, const void *const *src, int n, const double *w, void *out,
+                   int64_t numel, hipStream_t stream) {
+  if (numel == 0) return ok();
+  int cus = 0;
+  int rc = device_cus(&cus);
+  if (rc != CHEB_OK) return rc;
+  const cheb_launch_config cfg = launch_shape();
+  hipError_t e = dtype == CHEB_BF16
+                     ? launch_op<Bf16Op>(src, n, w, out, numel, cfg, cus, stream)
+                     : launch_op<F32Op>(src, n, w, out, numel, cfg, cus, stream);
+  if (e != hipSuccess) return fail(CHEB_E_HIP, "combine launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+int launch_gather(int dtype, void *slot_base, const GatherSeg *segs, int n_segs,
+                  hipStream_t stream) {
+  const int vec = elems_per_vec(dtype);
+  for (int first = 0; first < n_segs; first += kGatherMax) {
+    const int count = std::min(kGatherMax, n_segs - first);
+    GatherArgs a;
+    memset(&a, 0, sizeof a);
+    uint32_t blocks = 0;
+    int used = 0;
+    for (int j = 0; j < count; ++j) {
+      const GatherSeg &g = segs[first + j];
+      const uint64_t vecs = (uint64_t(g.numel) + vec - 1) / vec;
+      const uint64_t chunks = (vecs + kGatherChunk - 1) / kGatherChunk;
+      if (chunks == 0) continue;  // empty segment: nothing to copy
+      a.src[used] = g.src;
+      a.dst_offset[used] = uint64_t(g.dst_offset);
+      a.numel[used] = uint64_t(g.numel);
+      a.chunk_begin[used] = blocks;
+      blocks += uint32_t(chunks);
+      ++used;
+    }
+    if (used == 0) continue;
+    a.chunk_begin[used] = blocks;
+    a.n = used;
+    char *slot = static_cast<char *>(slot_base);
+    if (dtype == CHEB_BF16)
+      hipLaunchKernelGGL(gather_kernel<uint16_t>, dim3(blocks), dim3(kBlock), 0, stream, a, slot);
+    else
+      hipLaunchKernelGGL(gather_kernel<float>, dim3(blocks), dim3(kBlock), 0, stream, a, slot);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return fail(CHEB_E_HIP, "push launch failed: %s", hipGetErrorString(e));
+  }
+  return ok();
+}
+
+}  // namespace cheb

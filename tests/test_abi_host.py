@@ -1,0 +1,300 @@
+"""Host-side checks of libcheb through its C ABI (no GPU needed).
+
+The library validates every argument before it touches the HIP runtime, so
+everything here (exports, weights, layout, ring bookkeeping, error codes)
+runs on the CPU.  Calls that would enqueue GPU work are not made.
+"""
+import ctypes
+import math
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2608_23429_amd as cheb
+from paper_2608_23429_amd import _binding as B
+from synth import CONFIGS
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "cheb.h")
+FAKE_ARENA = 1 << 40      # 256-byte aligned address; never dereferenced here
+
+
+def _declared():
+    with open(HEADER) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"CHEB_API\s+[^;(]*?\b(cheb_\w+)\s*\(", text)))
+
+
+def test_header_declares_expected_entry_points():
+    names = _declared()
+    for must in ("cheb_precompute_weights", "cheb_cache_push", "cheb_extrapolate",
+                 "cheb_cache_create", "cheb_last_error"):
+        assert must in names
+    assert len(names) == len(B.SIGNATURES)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(B.LIB_PATH)
+    for name in _declared():
+        assert hasattr(lib, name), name
+        assert name in B.SIGNATURES, name
+        assert hasattr(cheb, name), name       # same name in the binding
+
+
+def test_version():
+    assert cheb.cheb_version() == 1
+
+
+def _wtol(w, factor=8.0):
+    s = float(np.abs(w).sum())
+    return factor * len(w) * 2.0 ** -53 * s * max(s, 1.0)
+
+
+@pytest.mark.parametrize("cfg", CONFIGS, ids=lambda c: c.name)
+def test_weights_match_oracle_on_workloads(cfg):
+    cases = [(cfg.nodes, cfg.targets)]
+    if cfg.alt_nodes is not None:
+        cases.append((cfg.alt_nodes, cfg.alt_targets))
+    for nodes, targets in cases:
+        w = cheb.cheb_precompute_weights(nodes, targets)
+        ref = oracle.weights(nodes, targets)
+        for m in range(len(targets)):
+            assert np.max(np.abs(w[m] - ref[m])) <= _wtol(ref[m]), (cfg.name, targets[m])
+
+
+def test_weights_match_oracle_random():
+    rng = np.random.default_rng(101)
+    for n in range(1, 9):
+        for _ in range(40):
+            x = rng.uniform(-50, 50, n)
+            if n > 1 and np.min(np.diff(np.sort(x))) < 1.0:
+                continue
+            t = rng.uniform(-80, 80, 3)
+            w = cheb.cheb_precompute_weights(x, t)
+            ref = oracle.weights(x, t)
+            for m in range(3):
+                assert np.max(np.abs(w[m] - ref[m])) <= _wtol(ref[m], 32.0)
+
+
+def test_weights_node_hit_and_single_node():
+    x = [0.96, 0.9, 0.8, 0.72, 0.6, 0.5]
+    w = cheb.cheb_precompute_weights(x, x)
+    assert np.array_equal(w, np.eye(6))
+    assert cheb.cheb_precompute_weights([3.0], [1.0, 7.0]).tolist() == [[1.0], [1.0]]
+
+
+def test_weights_errors_leave_output_untouched():
+    h = np.array([1.0, 2.0, 1.0])
+    t = np.array([4.0])
+    w = np.full((1, 3), 7.0)
+    rc = B.LIB.cheb_precompute_weights(B._dptr(h), 3, B._dptr(t), 1, B._dptr(w))
+    assert rc == B.CHEB_E_DUPNODE
+    assert np.all(w == 7.0)
+    assert "equal" in cheb.cheb_last_error()
+    with pytest.raises(cheb.ChebError) as e:
+        cheb.cheb_precompute_weights([1.0, np.nan], [3.0])
+    assert e.value.code == B.CHEB_E_NONFINITE
+    with pytest.raises(cheb.ChebError) as e:
+        cheb.cheb_precompute_weights([1.0, 2.0], [np.inf])
+    assert e.value.code == B.CHEB_E_NONFINITE
+    with pytest.raises(cheb.ChebError) as e:
+        cheb.cheb_precompute_weights([], [1.0])
+    assert e.value.code == B.CHEB_E_INVAL
+    with pytest.raises(cheb.ChebError) as e:
+        cheb.cheb_precompute_weights(np.arange(65.0), [100.0])
+    assert e.value.code == B.CHEB_E_INVAL
+    assert cheb.cheb_precompute_weights(np.arange(64.0), []).shape == (0, 64)
+
+
+# --------------------------------------------------------------------------
+# Layout
+# --------------------------------------------------------------------------
+
+def _expected_layout(n_slots, esize, seg):
+    vec = 16 // esize
+    off, pos = [], 0
+    for n in seg:
+        off.append(pos)
+        pos += -(-n // vec) * vec
+    stride = -(-(pos * esize) // 256) * 256
+    return off, pos, stride, stride * n_slots
+
+
+@pytest.mark.parametrize("dtype,esize", [(B.CHEB_BF16, 2), (B.CHEB_F32, 4)])
+def test_layout_rounding(dtype, esize):
+    seg = [1, 8, 13, 0, 1000003, 3, 4096 * 3072]
+    lay = cheb.cheb_cache_layout(5, dtype, seg)
+    off, pos, stride, arena = _expected_layout(5, esize, seg)
+    assert lay["seg_offset"].tolist() == off
+    assert lay["slot_numel"] == pos
+    assert lay["slot_stride_bytes"] == stride and stride % 256 == 0
+    assert lay["arena_bytes"] == arena
+
+
+def test_layout_of_workloads_has_no_padding():
+    for c in CONFIGS:
+        lay = cheb.cheb_cache_layout(c.n_hist, B.CHEB_BF16 if c.dtype == "bf16" else B.CHEB_F32,
+                                     c.seg_numel)
+        assert lay["slot_numel"] == c.numel
+        assert lay["seg_offset"].tolist() == list(np.cumsum([0] + c.seg_numel[:-1]))
+
+
+def test_layout_errors():
+    for args, code in [((0, 0, [4]), B.CHEB_E_INVAL), ((9, 0, [4]), B.CHEB_E_INVAL),
+                       ((2, 5, [4]), B.CHEB_E_DTYPE), ((2, 0, [-1]), B.CHEB_E_INVAL),
+                       ((2, 0, [1 << 40]), B.CHEB_E_INVAL)]:
+        with pytest.raises(cheb.ChebError) as e:
+            cheb.cheb_cache_layout(*args)
+        assert e.value.code == code
+
+
+# --------------------------------------------------------------------------
+# Ring bookkeeping (metadata paths only; no GPU work is enqueued)
+# --------------------------------------------------------------------------
+
+def _fake_cache(n_slots=4, seg=(1000, 24), dtype=B.CHEB_BF16):
+    lay = cheb.cheb_cache_layout(n_slots, dtype, list(seg))
+    h = cheb.cheb_cache_create(n_slots, dtype, list(seg), FAKE_ARENA, lay["arena_bytes"])
+    return h, lay
+
+
+def test_create_errors():
+    lay = cheb.cheb_cache_layout(4, B.CHEB_BF16, [1000])
+    with pytest.raises(cheb.ChebError) as e:
+        cheb.cheb_cache_create(4, B.CHEB_BF16, [1000], FAKE_ARENA + 16, lay["arena_bytes"])
+    assert e.value.code == B.CHEB_E_ALIGN
+    with pytest.raises(cheb.ChebError) as e:
+        cheb.cheb_cache_create(4, B.CHEB_BF16, [1000], FAKE_ARENA, lay["arena_bytes"] - 1)
+    assert e.value.code == B.CHEB_E_MISMATCH
+    with pytest.raises(cheb.ChebError) as e:
+        cheb.cheb_cache_create(4, B.CHEB_BF16, [1000], 0, lay["arena_bytes"])
+    assert e.value.code == B.CHEB_E_INVAL
+
+
+def test_fifo_order_and_eviction():
+    """Algorithm 1: H holds the n most recent (s, f_s); the oldest is dropped."""
+    h, lay = _fake_cache(n_slots=4)
+    stride = lay["slot_stride_bytes"]
+    seen = []
+    for i, t in enumerate([999.0, 979.0, 959.0, 939.0, 919.0, 899.0, 879.0]):
+        base = cheb.cheb_cache_begin_push(h)
+        assert base == FAKE_ARENA + (i % 4) * stride      # slots reused round robin
+        cheb.cheb_cache_commit(h, t)
+        seen.append(t)
+        hist = cheb.cheb_cache_history(h)
+        assert hist.tolist() == seen[-4:]
+        for age in range(len(hist)):
+            j = len(seen) - len(hist) + age            # push index of this entry
+            assert cheb.cheb_cache_entry(h, age) == FAKE_ARENA + (j % 4) * stride
+    cheb.cheb_cache_reset(h)
+    assert cheb.cheb_cache_history(h).size == 0
+    cheb.cheb_cache_destroy(h)
+
+
+def test_not_ready_until_full_and_while_push_open():
+    h, lay = _fake_cache(n_slots=3)
+    out = FAKE_ARENA + 4 * lay["arena_bytes"]
+    for t in [1.0, 2.0]:
+        with pytest.raises(cheb.ChebError) as e:
+            cheb.cheb_extrapolate(h, [0.2, 0.3, 0.5], out)
+        assert e.value.code == B.CHEB_E_NOTREADY
+        with pytest.raises(cheb.ChebError) as e:
+            cheb.cheb_extrapolate_at(h, 9.0, out)
+        assert e.value.code == B.CHEB_E_NOTREADY
+        cheb.cheb_cache_begin_push(h)
+        cheb.cheb_cache_commit(h, t)
+    cheb.cheb_cache_begin_push(h)
+    with pytest.raises(cheb.ChebError) as e:
+        cheb.cheb_extrapolate(h, [0.2, 0.3, 0.5], out)
+    assert e.value.code == B.CHEB_E_NOTREADY
+    with pytest.raises(cheb.ChebError) as e:
+        cheb.cheb_cache_begin_push(h)
+    assert e.value.code == B.CHEB_E_NOTREADY
+    with pytest.raises(cheb.ChebError) as e:
+        cheb.cheb_cache_push(h, 5.0, [FAKE_ARENA * 2, FAKE_ARENA * 3])
+    assert e.value.code == B.CHEB_E_NOTREADY
+    cheb.cheb_cache_commit(h, 3.0)
+    with pytest.raises(cheb.ChebError) as e:
+        cheb.cheb_cache_commit(h, 4.0)
+    assert e.value.code == B.CHEB_E_NOTREADY
+    cheb.cheb_cache_destroy(h)
+
+
+def test_duplicate_abscissa_rules():
+    h, _ = _fake_cache(n_slots=3)
+    for t in [10.0, 20.0, 30.0]:
+        cheb.cheb_cache_begin_push(h)
+        cheb.cheb_cache_commit(h, t)
+    # Full: the next push drops 10, so 10 may come back but 20 may not.
+    cheb.cheb_cache_begin_push(h)
+    with pytest.raises(cheb.ChebError) as e:
+        cheb.cheb_cache_commit(h, 20.0)
+    assert e.value.code == B.CHEB_E_DUPNODE
+    with pytest.raises(cheb.ChebError) as e:
+        cheb.cheb_cache_commit(h, float("nan"))
+    assert e.value.code == B.CHEB_E_NONFINITE
+    cheb.cheb_cache_commit(h, 10.0)
+    assert cheb.cheb_cache_history(h).tolist() == [20.0, 30.0, 10.0]
+    cheb.cheb_cache_destroy(h)
+
+
+def test_push_validation_before_launch():
+    h, _ = _fake_cache(n_slots=2, seg=(1000, 24))
+    with pytest.raises(cheb.ChebError) as e:
+        cheb.cheb_cache_push(h, 1.0, [FAKE_ARENA * 2 + 8, FAKE_ARENA * 3])
+    assert e.value.code == B.CHEB_E_ALIGN
+    with pytest.raises(cheb.ChebError) as e:
+        cheb.cheb_cache_push(h, 1.0, [0, FAKE_ARENA * 3])
+    assert e.value.code == B.CHEB_E_INVAL
+    with pytest.raises(cheb.ChebError) as e:
+        cheb.cheb_cache_push(h, float("inf"), [FAKE_ARENA * 2, FAKE_ARENA * 3])
+    assert e.value.code == B.CHEB_E_NONFINITE
+    assert cheb.cheb_cache_history(h).size == 0     # nothing recorded
+    cheb.cheb_cache_destroy(h)
+
+
+def test_segment_offsets_and_slot_numel():
+    h, lay = _fake_cache(n_slots=2, seg=(5, 17, 8))
+    assert [cheb.cheb_cache_segment_offset(h, s) for s in range(3)] == lay["seg_offset"].tolist()
+    assert cheb.cheb_cache_slot_numel(h) == lay["slot_numel"] == 8 + 24 + 8
+    with pytest.raises(cheb.ChebError):
+        cheb.cheb_cache_segment_offset(h, 3)
+    with pytest.raises(cheb.ChebError):
+        cheb.cheb_cache_entry(h, 0)
+    cheb.cheb_cache_destroy(h)
+
+
+def test_combine_validation_before_launch():
+    a, b, o = FAKE_ARENA, FAKE_ARENA + (1 << 30), FAKE_ARENA + (2 << 30)
+    cases = [
+        (([a, b], [0.5, 0.5], o, 100, 7), B.CHEB_E_DTYPE),
+        (([], [], o, 100, 0), B.CHEB_E_INVAL),
+        (([a] * 9, [0.1] * 9, o, 100, 0), B.CHEB_E_INVAL),
+        (([a + 2, b], [0.5, 0.5], o, 100, 0), B.CHEB_E_ALIGN),
+        (([a, b], [0.5, 0.5], o + 4, 100, 0), B.CHEB_E_ALIGN),
+        (([a, b], [0.5, float("nan")], o, 100, 0), B.CHEB_E_NONFINITE),
+        (([a, b], [0.5, 0.5], a + 64, 100, 0), B.CHEB_E_INVAL),      # overlap
+        (([a, b], [0.5, 0.5], o, -1, 0), B.CHEB_E_INVAL),
+        (([a, b], [0.5, 0.5], o, 1 << 34, 0), B.CHEB_E_INVAL),
+        (([a, 0], [0.5, 0.5], o, 100, 0), B.CHEB_E_INVAL),
+    ]
+    for args, code in cases:
+        with pytest.raises(cheb.ChebError) as e:
+            cheb.cheb_combine(*args)
+        assert e.value.code == code, (args, e.value)
+    cheb.cheb_combine([a, b], [0.5, 0.5], o, 0, 0)          # empty: no work, OK
+
+
+def test_launch_config_roundtrip_and_validation():
+    old = cheb.cheb_get_launch_config()
+    try:
+        cheb.cheb_set_launch_config(2, 0, 8)
+        assert cheb.cheb_get_launch_config() == {"unroll": 2, "nontemporal": 0, "blocks_per_cu": 8}
+        for bad in [(3, 1, 0), (4, 2, 0), (4, 1, -1), (4, 1, 65)]:
+            with pytest.raises(cheb.ChebError):
+                cheb.cheb_set_launch_config(*bad)
+    finally:
+        cheb.cheb_set_launch_config(**old)

@@ -1,0 +1,297 @@
+"""GPU parity of libcheb against the fp64 CPU oracle, through the C ABI.
+
+Inputs are seeded and drawn once on the device; the oracle gets exact host
+copies of the same stored values.  Floating-point results must satisfy the
+floored relative bound (1e-2 for bfloat16 storage, 1e-5 for float32 storage);
+bit patterns are compared exactly where the result is fixed bit for bit.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_23429_amd as cheb
+from synth import CONFIGS, make_history, split_segments
+from tests.gpu_util import TOL, check_parity, decode, say, to_host_bits
+
+pytestmark = pytest.mark.gpu
+
+DT = {"bf16": torch.bfloat16, "f32": torch.float32}
+SHAPES = [
+    {"unroll": 4, "nontemporal": 1, "blocks_per_cu": 0},
+    {"unroll": 1, "nontemporal": 0, "blocks_per_cu": 0},
+    {"unroll": 2, "nontemporal": 1, "blocks_per_cu": 0},
+    {"unroll": 4, "nontemporal": 0, "blocks_per_cu": 2},
+    {"unroll": 2, "nontemporal": 1, "blocks_per_cu": 8},
+]
+
+
+@pytest.fixture(autouse=True)
+def _default_shape():
+    old = cheb.cheb_get_launch_config()
+    yield
+    cheb.cheb_set_launch_config(**old)
+    torch.cuda.synchronize()
+
+
+def _rand(n, numel, dtype, seed, scale=1.0):
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    return [(torch.randn(numel, generator=g, device="cuda") * scale).to(DT[dtype])
+            for _ in range(n)]
+
+
+# --------------------------------------------------------------------------
+# Stateless combination: every history size, ragged sizes, every launch shape
+# --------------------------------------------------------------------------
+
+NUMELS = [1, 7, 8, 9, 255, 1000, 65536 + 13, 3 * 4 * 256 * 8 + 5, 1 << 20]
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("n", range(1, 9))
+def test_combine_all_sizes(dtype, n):
+    rng = np.random.default_rng(1000 + n)
+    for numel in NUMELS:
+        say(f"combine dtype={dtype} n={n} numel={numel}")
+        srcs = _rand(n, numel, dtype, seed=numel * 31 + n)
+        # extrapolation-like weights: from equispaced nodes, target ahead
+        w = oracle.weights_row(np.arange(n, dtype=float), n - 1 + rng.uniform(0.1, 2.0))
+        out = torch.empty(numel, dtype=DT[dtype], device="cuda")
+        cheb.combine(srcs, w, out)
+        torch.cuda.synchronize()
+        check_parity(to_host_bits(out), [to_host_bits(s) for s in srcs], w, dtype,
+                     f"n={n} numel={numel}")
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "u{unroll}_nt{nontemporal}_b{blocks_per_cu}".format(**s))
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_combine_launch_shapes(shape, dtype):
+    cheb.cheb_set_launch_config(**shape)
+    n = 6
+    for numel in [5, 4096 * 8 + 3, 2_000_003]:
+        say(f"shape={shape} dtype={dtype} numel={numel}")
+        srcs = _rand(n, numel, dtype, seed=numel)
+        w = oracle.weights_row([2, 5, 10, 14, 20, 25], 27)
+        out = torch.empty(numel, dtype=DT[dtype], device="cuda")
+        cheb.combine(srcs, w, out)
+        torch.cuda.synchronize()
+        check_parity(to_host_bits(out), [to_host_bits(s) for s in srcs], w, dtype, str(shape))
+
+
+def test_combine_empty_and_nonzero_stream():
+    out = torch.empty(0, dtype=torch.bfloat16, device="cuda")
+    cheb.combine([out, out], [0.5, 0.5], out)
+    s = torch.cuda.Stream()
+    srcs = _rand(3, 300_001, "bf16", seed=5)
+    out = torch.empty(300_001, dtype=torch.bfloat16, device="cuda")
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s):
+        cheb.combine(srcs, [0.25, -1.0, 1.75], out, stream=s)
+    s.synchronize()
+    check_parity(to_host_bits(out), [to_host_bits(x) for x in srcs], [0.25, -1.0, 1.75], "bf16")
+
+
+# --------------------------------------------------------------------------
+# Bit-exact special cases
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_unit_weights_copy_bitwise(dtype):
+    """w = e_j: every output is entry j's stored value (K = 0 is the n = 1 case)."""
+    numel = 123_457
+    for n in (1, 4, 6, 8):
+        srcs = _rand(n, numel, dtype, seed=77 + n)
+        for j in range(n):
+            w = np.zeros(n)
+            w[j] = 1.0
+            out = torch.empty(numel, dtype=DT[dtype], device="cuda")
+            cheb.combine(srcs, w, out)
+            torch.cuda.synchronize()
+            got = decode(to_host_bits(out), dtype)
+            ref = decode(to_host_bits(srcs[j]), dtype)
+            assert np.array_equal(got, ref), (n, j)
+
+
+def test_bf16_midpoint_weights_round_to_nearest_even():
+    """w = (1/2, 1/2) on bfloat16 inputs in [1, 2): the fp32 sum is
+    exact, so the output must be the correctly rounded bfloat16 of the exact
+    mean, which the oracle's rounding routine gives bit for bit."""
+    numel = 1 << 18
+    g = torch.Generator(device="cuda")
+    g.manual_seed(3)
+    a = ((torch.rand(numel, generator=g, device="cuda") + 1.0)).to(torch.bfloat16)
+    b = ((torch.rand(numel, generator=g, device="cuda") + 1.0)).to(torch.bfloat16)
+    out = torch.empty(numel, dtype=torch.bfloat16, device="cuda")
+    cheb.combine([a, b], [0.5, 0.5], out)
+    torch.cuda.synchronize()
+    ha, hb = to_host_bits(a), to_host_bits(b)
+    exact = 0.5 * oracle.bf16_to_f64(ha) + 0.5 * oracle.bf16_to_f64(hb)
+    expect = oracle.round_bf16(exact)
+    got = to_host_bits(out)
+    assert np.array_equal(got, expect)
+    # ties really occur in this input, so the even rule is exercised
+    # (inputs are multiples of 2^-7, so a tie is an odd multiple of 2^-8)
+    ties = np.mod(exact * 256.0, 2.0) == 1.0
+    assert ties.any()
+
+
+# --------------------------------------------------------------------------
+# History ring on the device
+# --------------------------------------------------------------------------
+
+RAGGED = [13, 1, 8, 1_000_003, 0, 4096 * 3 + 7]
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_ring_push_eviction_and_padding(dtype):
+    n = 4
+    cache = cheb.ChebCache(n, DT[dtype], RAGGED)
+    pushed = []
+    ts = [999.0, 979.0, 959.0, 939.0, 919.0, 899.0, 879.0]
+    for i, t in enumerate(ts):
+        say(f"ring dtype={dtype} push {i}")
+        segs = []
+        for s, m in enumerate(RAGGED):
+            g = torch.Generator(device="cuda")
+            g.manual_seed(100 * i + s)
+            segs.append(torch.randn(m, generator=g, device="cuda").to(DT[dtype]))
+        cache.push(t, segs)
+        pushed.append((t, segs))
+        torch.cuda.synchronize()
+        held = pushed[-n:]
+        assert cache.history().tolist() == [p[0] for p in held]
+        for age, (_, psegs) in enumerate(held):
+            flat = to_host_bits(cache.entry(age))
+            for s, (off, m) in enumerate(zip(cache.seg_offset, cache.seg_numel)):
+                assert np.array_equal(flat[off:off + m], to_host_bits(psegs[s])), (i, age, s)
+                end = off + m
+                pad_end = -(-m // (8 if dtype == "bf16" else 4)) * (8 if dtype == "bf16" else 4) + off
+                assert np.all(flat[end:pad_end] == 0), "padding not zeroed"
+    # Prediction over the held entries, per segment, against the oracle.
+    out, w = cache.extrapolate_at(859.0)
+    torch.cuda.synchronize()
+    w_or = oracle.weights_row(cache.history(), 859.0)
+    assert np.max(np.abs(w - w_or)) <= 1e-12 * np.abs(w_or).sum() ** 2
+    got = to_host_bits(out)
+    hosts = [to_host_bits(cache.entry(a)) for a in range(n)]
+    for s, (off, m) in enumerate(zip(cache.seg_offset, cache.seg_numel)):
+        check_parity(got[off:off + m], [h[off:off + m] for h in hosts], w_or, dtype, f"seg{s}")
+    cache.close()
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_fused_push_matches_copy_push(dtype):
+    seg = [4096 * 8, 1000, 24]
+    a = cheb.ChebCache(3, DT[dtype], seg)
+    b = cheb.ChebCache(3, DT[dtype], seg)
+    for i, t in enumerate([0.96, 0.9, 0.8, 0.72]):
+        segs = [(_rand(1, m, dtype, seed=10 * i + k)[0]) for k, m in enumerate(seg)]
+        a.push(t, segs)
+        slot = b.begin_push()
+        for view, src in zip(b.segment_views(slot), segs):
+            view.copy_(src)
+        b.commit(t)
+    torch.cuda.synchronize()
+    assert a.history().tolist() == b.history().tolist() == [0.9, 0.8, 0.72]
+    oa, _ = a.extrapolate_at(0.6)
+    ob, _ = b.extrapolate_at(0.6)
+    torch.cuda.synchronize()
+    for va, vb in zip(a.segment_views(oa), b.segment_views(ob)):
+        assert torch.equal(va.view(torch.int16 if dtype == "bf16" else torch.int32),
+                           vb.view(torch.int16 if dtype == "bf16" else torch.int32))
+    a.close()
+    b.close()
+
+
+# --------------------------------------------------------------------------
+# The five workloads
+# --------------------------------------------------------------------------
+
+def _run_workload(cfg, nodes, targets, time_scale=None, label=""):
+    """Seeded history on the device -> push through the ring -> one
+    prediction per target; returns (cache, entries, outputs, weights)."""
+    entries = make_history(cfg, "cuda", nodes=nodes, time_scale=time_scale)
+    cache = cheb.ChebCache(cfg.n_hist, DT[cfg.dtype], cfg.seg_numel)
+    for x, e in zip(nodes, entries):
+        cache.push(x, split_segments(e, cfg))
+    outs, ws = [], []
+    for t in targets:
+        out, w = cache.extrapolate_at(t)
+        outs.append(out)
+        ws.append(w)
+    torch.cuda.synchronize()
+    return cache, entries, outs, ws
+
+
+@pytest.mark.parametrize("cfg", CONFIGS, ids=lambda c: c.name)
+def test_workload_small_all_elements(cfg):
+    """Each workload's schedule and generator on a cache cut down so the
+    oracle checks every element (ragged segment mix kept)."""
+    small = cfg.shrunk(600_000)
+    readings = [(small.nodes, small.targets, None)]
+    if small.alt_nodes is not None:
+        readings.append((small.alt_nodes, small.alt_targets,
+                         20.0 if cfg.name.startswith("pixart") else None))
+    for nodes, targets, ts in readings:
+        say(f"workload {cfg.name} (small, {small.numel} elems) nodes={nodes}")
+        cache, entries, outs, ws = _run_workload(small, nodes, targets, ts)
+        hosts = [to_host_bits(e) for e in entries]
+        for t, out, w in zip(targets, outs, ws):
+            w_or = oracle.weights_row(nodes, t)
+            check_parity(to_host_bits(out), hosts, w_or, small.dtype, f"{cfg.name} t={t}")
+        cache.close()
+        del entries, outs
+    torch.cuda.empty_cache()
+
+
+def _sample_indices(numel, seg_offsets, seg_numel, count, seed):
+    rng = np.random.default_rng(seed)
+    idx = [rng.integers(0, numel, size=count)]
+    idx.append(np.arange(min(4096, numel)))
+    idx.append(np.arange(max(0, numel - 4096), numel))
+    for off, m in zip(seg_offsets, seg_numel):       # both ends of every segment
+        idx.append(np.arange(off, off + min(16, m)))
+        idx.append(np.arange(max(off, off + m - 16), off + m))
+    return np.unique(np.concatenate(idx))
+
+
+@pytest.mark.parametrize("cfg", CONFIGS, ids=lambda c: c.name)
+def test_workload_full_size_sampled(cfg):
+    """Full cache shape, default launch shape (the one the benchmark times):
+    the oracle recomputes a sample of outputs (random elements, both ends of
+    the cache and of every segment) from the same stored inputs."""
+    cheb.cheb_set_launch_config(unroll=4, nontemporal=1, blocks_per_cu=0)
+    say(f"workload {cfg.name} full size: {cfg.numel} elements x {cfg.n_hist}")
+    cache, entries, outs, ws = _run_workload(cfg, cfg.nodes, cfg.targets)
+    idx = _sample_indices(cfg.numel, cache.seg_offset, cache.seg_numel, 1 << 20, cfg.seed)
+    idx_t = torch.from_numpy(idx).to("cuda")
+    hosts = [to_host_bits(e.index_select(0, idx_t)) for e in entries]
+    for t, out in zip(cfg.targets, outs):
+        w_or = oracle.weights_row(cfg.nodes, t)
+        got = to_host_bits(out.index_select(0, idx_t))
+        e, nw = check_parity(got, hosts, w_or, cfg.dtype, f"{cfg.name} t={t}")
+        say(f"  t={t}: floored error {e:.3e}, normwise {nw:.3e}, {idx.size} samples")
+    cache.close()
+    del entries, outs, cache
+    torch.cuda.empty_cache()
+
+
+def test_tiny_recovers_quadratic():
+    """Tiny workload: F_k = A + B tau + C tau^2 + 1e-3 noise, stored in fp32.
+    The prediction at the next timesteps equals the quadratic at the target
+    up to the combined noise (|w| sums to at most 2.14 here) and fp32
+    storage rounding."""
+    cfg = CONFIGS[0]
+    cache, entries, outs, ws = _run_workload(cfg, cfg.nodes, cfg.targets)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(cfg.seed)
+    coeffs = [torch.randn(cfg.numel, generator=g, device="cuda") * cfg.coeff_std
+              for _ in range(cfg.degree + 1)]
+    for t, out, w in zip(cfg.targets, outs, ws):
+        tau = t / cfg.time_scale
+        quad = (coeffs[0].double() + coeffs[1].double() * tau + coeffs[2].double() * tau * tau)
+        dev = (out.double() - quad).abs().max().item()
+        bound = 6 * cfg.noise_std * float(np.abs(w).sum()) + 1e-5
+        assert dev <= bound, (t, dev, bound)
+    cache.close()
