@@ -59,6 +59,7 @@ def parse_args(argv=None):
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="flux_dev_1024")
+    ap.add_argument("--block", type=int, default=None)
     ap.add_argument("--unroll", type=int, default=None)
     ap.add_argument("--nontemporal", type=int, default=None)
     ap.add_argument("--blocks-per-cu", type=int, default=None)
@@ -238,7 +239,7 @@ def main(argv=None):
         return 0
 
     shape = cheb.cheb_get_launch_config()
-    for k, v in (("unroll", args.unroll), ("nontemporal", args.nontemporal),
+    for k, v in (("block", args.block), ("unroll", args.unroll), ("nontemporal", args.nontemporal),
                  ("blocks_per_cu", args.blocks_per_cu)):
         if v is not None:
             shape[k] = v

@@ -224,15 +224,18 @@ CHEB_API int cheb_extrapolate_at(cheb_cache *c, double target_t, void *out,
 /* ------------------------------------------------------------------------ */
 
 /* Launch shape of the streaming kernels, process-wide.
- *   unroll       16-byte vectors per thread per history entry in flight
- *                (1, 2 or 4).
+ *   block        threads per block: 256, 512 or 1024.
+ *   unroll       16-byte vectors per thread per history entry in flight;
+ *                block * unroll must not exceed 1024 (256: 1, 2 or 4;
+ *                512: 1 or 2; 1024: 1).
  *   nontemporal  1: history loads and output stores carry the non-temporal
  *                hint; 0: ordinary loads and stores.
- *   blocks_per_cu  0: one block per tile of 256 x unroll vectors (the grid
- *                covers the whole problem); > 0: a persistent grid of that
+ *   blocks_per_cu  0: one block per tile of block x unroll vectors (the grid
+ *                covers the whole problem); 1..64: a persistent grid of that
  *                many blocks per compute unit, each looping over tiles.
- * Errors: CHEB_E_INVAL. */
+ * Default {1024, 1, 1, 0}.  Errors: CHEB_E_INVAL. */
 typedef struct cheb_launch_config {
+  int32_t block;
   int32_t unroll;
   int32_t nontemporal;
   int32_t blocks_per_cu;

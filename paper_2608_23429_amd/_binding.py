@@ -43,8 +43,8 @@ class ChebError(RuntimeError):
 
 
 class cheb_launch_config(ctypes.Structure):
-    _fields_ = [("unroll", ctypes.c_int32), ("nontemporal", ctypes.c_int32),
-                ("blocks_per_cu", ctypes.c_int32)]
+    _fields_ = [("block", ctypes.c_int32), ("unroll", ctypes.c_int32),
+                ("nontemporal", ctypes.c_int32), ("blocks_per_cu", ctypes.c_int32)]
 
 
 _dp = ctypes.POINTER(ctypes.c_double)
@@ -224,9 +224,10 @@ def cheb_extrapolate_at(handle, target_t, out_ptr, stream=0, n_slots=CHEB_MAX_SL
 def cheb_get_launch_config():
     c = cheb_launch_config()
     _check(LIB.cheb_get_launch_config(ctypes.byref(c)))
-    return {"unroll": c.unroll, "nontemporal": c.nontemporal, "blocks_per_cu": c.blocks_per_cu}
+    return {"block": c.block, "unroll": c.unroll, "nontemporal": c.nontemporal,
+            "blocks_per_cu": c.blocks_per_cu}
 
 
-def cheb_set_launch_config(unroll=4, nontemporal=1, blocks_per_cu=0):
-    c = cheb_launch_config(int(unroll), int(nontemporal), int(blocks_per_cu))
+def cheb_set_launch_config(block=1024, unroll=1, nontemporal=1, blocks_per_cu=0):
+    c = cheb_launch_config(int(block), int(unroll), int(nontemporal), int(blocks_per_cu))
     _check(LIB.cheb_set_launch_config(ctypes.byref(c)))

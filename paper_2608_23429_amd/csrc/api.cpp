@@ -15,7 +15,7 @@ namespace {
 thread_local char g_error[512] = "";
 
 std::mutex g_shape_mutex;
-cheb_launch_config g_shape = {4, 1, 0};
+cheb_launch_config g_shape = {1024, 1, 1, 0};
 
 constexpr int kMaxDevices = 64;
 int g_cus[kMaxDevices] = {0};
@@ -136,8 +136,13 @@ int cheb_get_launch_config(cheb_launch_config *cfg) {
 
 int cheb_set_launch_config(const cheb_launch_config *cfg) {
   if (!cfg) return fail(CHEB_E_INVAL, "cfg is NULL");
+  if (cfg->block != 256 && cfg->block != 512 && cfg->block != 1024)
+    return fail(CHEB_E_INVAL, "block must be 256, 512 or 1024 (got %d)", cfg->block);
   if (cfg->unroll != 1 && cfg->unroll != 2 && cfg->unroll != 4)
     return fail(CHEB_E_INVAL, "unroll must be 1, 2 or 4 (got %d)", cfg->unroll);
+  if (cfg->block * cfg->unroll > 1024)
+    return fail(CHEB_E_INVAL, "block x unroll must not exceed 1024 (got %d x %d)", cfg->block,
+                cfg->unroll);
   if (cfg->nontemporal != 0 && cfg->nontemporal != 1)
     return fail(CHEB_E_INVAL, "nontemporal must be 0 or 1 (got %d)", cfg->nontemporal);
   if (cfg->blocks_per_cu < 0 || cfg->blocks_per_cu > 64)

@@ -29,7 +29,7 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
-constexpr int kBlock = 256;  // 4 waves of 64 lanes
+constexpr int kBlock = 256;  // gather kernel: 4 waves of 64 lanes
 
 template <bool NT>
 __device__ __forceinline__ u32x4 load16(const u32x4 *p) {
@@ -139,30 +139,33 @@ struct F32Op {
 
 // ---- the streaming kernel -------------------------------------------------
 //
-// The vector range [0, n_vec) is cut into tiles of kBlock * U vectors.  A
-// block takes tiles blockIdx.x, blockIdx.x + gridDim.x, ... (one tile per
-// block when the grid covers the range, a persistent loop otherwise).  In a
-// tile, lane t of the block handles vectors t, t + kBlock, ..., so every
-// load instruction of a wave reads 64 consecutive 16-byte vectors.
-template <class Op, int NS, int U, bool NT>
-__global__ __launch_bounds__(kBlock) void combine_kernel(Hist<NS, typename Op::W> h,
-                                                         u32x4 *__restrict__ out,
-                                                         uint32_t n_vec, uint32_t n_tiles,
-                                                         Tail tail) {
+// The vector range [0, n_vec) is cut into tiles of BLK * U vectors.  A block
+// takes tiles blockIdx.x, blockIdx.x + gridDim.x, ... (one tile per block
+// when the grid covers the range, a persistent loop otherwise).  In a tile,
+// lane t handles vectors t, t + BLK, ..., so every load instruction of a
+// wave reads 64 consecutive 16-byte vectors (1 KiB).  A scheduling barrier
+// keeps all NS x U loads of a thread ahead of its arithmetic, so each wave
+// has its whole working set in flight before it waits.
+template <class Op, int NS, int BLK, int U, bool NT>
+__global__ __launch_bounds__(BLK) void combine_kernel(Hist<NS, typename Op::W> h,
+                                                      u32x4 *__restrict__ out,
+                                                      uint32_t n_vec, uint32_t n_tiles,
+                                                      Tail tail) {
   for (uint32_t tile = blockIdx.x; tile < n_tiles; tile += gridDim.x) {
-    const uint32_t base = tile * uint32_t(kBlock * U) + threadIdx.x;
-    if (base + uint32_t((U - 1) * kBlock) < n_vec) {
+    const uint32_t base = tile * uint32_t(BLK * U) + threadIdx.x;
+    if (base + uint32_t((U - 1) * BLK) < n_vec) {
       u32x4 v[U][NS];
 #pragma unroll
       for (int u = 0; u < U; ++u)
 #pragma unroll
-        for (int k = 0; k < NS; ++k) v[u][k] = load16<NT>(h.p[k] + base + u * kBlock);
+        for (int k = 0; k < NS; ++k) v[u][k] = load16<NT>(h.p[k] + base + u * BLK);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int u = 0; u < U; ++u) store16<NT>(out + base + u * kBlock, Op::template vec<NS>(v[u], h.w));
+      for (int u = 0; u < U; ++u) store16<NT>(out + base + u * BLK, Op::template vec<NS>(v[u], h.w));
     } else {
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        const uint32_t i = base + u * kBlock;
+        const uint32_t i = base + u * BLK;
         if (i < n_vec) {
           u32x4 v[NS];
 #pragma unroll
@@ -182,16 +185,30 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(Hist<NS, typename Op::W
   }
 }
 
-template <class Op, int NS, int U, bool NT>
+template <class Op, int NS, int BLK, int U, bool NT>
 hipError_t launch_shape_ns(const Hist<NS, typename Op::W> &h, u32x4 *out, uint32_t n_vec,
                            Tail tail, int blocks_per_cu, int cus, hipStream_t s) {
-  const uint32_t per_tile = uint32_t(kBlock * U);
+  const uint32_t per_tile = uint32_t(BLK * U);
   const uint32_t n_tiles = (n_vec + per_tile - 1) / per_tile;
   uint32_t grid = std::max<uint32_t>(n_tiles, 1u);
   if (blocks_per_cu > 0) grid = std::min<uint32_t>(grid, uint32_t(blocks_per_cu) * uint32_t(cus));
-  hipLaunchKernelGGL((combine_kernel<Op, NS, U, NT>), dim3(grid), dim3(kBlock), 0, s, h, out,
+  hipLaunchKernelGGL((combine_kernel<Op, NS, BLK, U, NT>), dim3(grid), dim3(BLK), 0, s, h, out,
                      n_vec, n_tiles, tail);
   return hipGetLastError();
+}
+
+template <class Op, int NS, bool NT>
+hipError_t launch_nt(const Hist<NS, typename Op::W> &h, u32x4 *out, uint32_t n_vec, Tail tail,
+                     const cheb_launch_config &cfg, int cus, hipStream_t s) {
+  const int b = cfg.block, u = cfg.unroll, g = cfg.blocks_per_cu;
+  if (b == 1024) return launch_shape_ns<Op, NS, 1024, 1, NT>(h, out, n_vec, tail, g, cus, s);
+  if (b == 512) {
+    if (u == 1) return launch_shape_ns<Op, NS, 512, 1, NT>(h, out, n_vec, tail, g, cus, s);
+    return launch_shape_ns<Op, NS, 512, 2, NT>(h, out, n_vec, tail, g, cus, s);
+  }
+  if (u == 1) return launch_shape_ns<Op, NS, 256, 1, NT>(h, out, n_vec, tail, g, cus, s);
+  if (u == 2) return launch_shape_ns<Op, NS, 256, 2, NT>(h, out, n_vec, tail, g, cus, s);
+  return launch_shape_ns<Op, NS, 256, 4, NT>(h, out, n_vec, tail, g, cus, s);
 }
 
 template <class Op, int NS>
@@ -206,18 +223,8 @@ hipError_t launch_ns(const void *const *src, const double *w, void *out, int64_t
   const uint32_t n_vec = uint32_t(numel / kVec);
   Tail tail{uint32_t(numel % kVec), uint64_t(numel / kVec) * kVec};
   u32x4 *o = static_cast<u32x4 *>(out);
-  const bool nt = cfg.nontemporal != 0;
-  switch (cfg.unroll) {
-    case 1:
-      return nt ? launch_shape_ns<Op, NS, 1, true>(h, o, n_vec, tail, cfg.blocks_per_cu, cus, s)
-                : launch_shape_ns<Op, NS, 1, false>(h, o, n_vec, tail, cfg.blocks_per_cu, cus, s);
-    case 2:
-      return nt ? launch_shape_ns<Op, NS, 2, true>(h, o, n_vec, tail, cfg.blocks_per_cu, cus, s)
-                : launch_shape_ns<Op, NS, 2, false>(h, o, n_vec, tail, cfg.blocks_per_cu, cus, s);
-    default:
-      return nt ? launch_shape_ns<Op, NS, 4, true>(h, o, n_vec, tail, cfg.blocks_per_cu, cus, s)
-                : launch_shape_ns<Op, NS, 4, false>(h, o, n_vec, tail, cfg.blocks_per_cu, cus, s);
-  }
+  return cfg.nontemporal ? launch_nt<Op, NS, true>(h, o, n_vec, tail, cfg, cus, s)
+                         : launch_nt<Op, NS, false>(h, o, n_vec, tail, cfg, cus, s);
 }
 
 template <class Op>

@@ -290,11 +290,15 @@ def test_combine_validation_before_launch():
 
 def test_launch_config_roundtrip_and_validation():
     old = cheb.cheb_get_launch_config()
+    assert old == {"block": 1024, "unroll": 1, "nontemporal": 1, "blocks_per_cu": 0}
     try:
-        cheb.cheb_set_launch_config(2, 0, 8)
-        assert cheb.cheb_get_launch_config() == {"unroll": 2, "nontemporal": 0, "blocks_per_cu": 8}
-        for bad in [(3, 1, 0), (4, 2, 0), (4, 1, -1), (4, 1, 65)]:
+        cheb.cheb_set_launch_config(256, 2, 0, 8)
+        assert cheb.cheb_get_launch_config() == {"block": 256, "unroll": 2, "nontemporal": 0,
+                                                 "blocks_per_cu": 8}
+        for bad in [(256, 3, 1, 0), (256, 4, 2, 0), (256, 4, 1, -1), (256, 4, 1, 65),
+                    (128, 1, 1, 0), (512, 4, 1, 0), (1024, 2, 1, 0)]:
             with pytest.raises(cheb.ChebError):
                 cheb.cheb_set_launch_config(*bad)
+        assert cheb.cheb_get_launch_config()["block"] == 256     # unchanged by failures
     finally:
         cheb.cheb_set_launch_config(**old)
