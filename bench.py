@@ -140,6 +140,31 @@ def time_steps(torch, cache, targets, out, steps, warmup):
     return region_ms, per
 
 
+def time_multi(torch, cfg, cache, steps, warmup):
+    """All skipped steps between two full steps (the workload's targets) from
+    one pass over the history: cheb_extrapolate_at_multi."""
+    stream = torch.cuda.current_stream()
+    outs = [cache.new_output() for _ in cfg.targets]
+    for _ in range(warmup):
+        cache.extrapolate_at_multi(cfg.targets, outs, stream=stream)
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for _ in range(steps):
+        cache.extrapolate_at_multi(cfg.targets, outs, stream=stream)
+    end.record(stream)
+    end.synchronize()
+    ms = start.elapsed_time(end) / steps
+    M = len(cfg.targets)
+    B = (cfg.n_hist + M) * cfg.numel * cfg.elem_size
+    del outs
+    return {"targets_per_pass": M, "us_per_pass": ms * 1e3, "us_per_skipped_step": ms * 1e3 / M,
+            "bytes_per_pass": B, "gbps": B / (ms * 1e6),
+            "note": "the workload's skipped steps between two full steps predicted in one "
+                    "pass over the history (cheb_extrapolate_at_multi); not in value"}
+
+
 def parity_sample(torch, cfg, entries, cache, out, target, count=1 << 16):
     import numpy as np
     import oracle
@@ -250,6 +275,9 @@ def main(argv=None):
         f"{args.warmup} warmup + {args.steps} timed steps")
     res, entries, cache, out = measure_config(torch, cheb, cfg, args.steps, args.warmup)
     log(f"[bench] {cfg.name}: {res['us_per_step']:.1f} us/step, {res['gbps']:.0f} GB/s")
+    multi = time_multi(torch, cfg, cache, max(10, args.steps // 2), args.warmup)
+    log(f"[bench] {cfg.name} multi-target: {multi['us_per_skipped_step']:.1f} us per skipped "
+        f"step ({multi['gbps']:.0f} GB/s over {multi['targets_per_pass']} targets)")
     par = parity_sample(torch, cfg, entries, cache, out, cfg.targets[-1])
     log(f"[bench] parity sample: floored error {par['floored_rel_err']:.3e}")
     achieved = res["bytes_per_step"] / (res["launch_us_avg"] * 1e3)
@@ -279,6 +307,7 @@ def main(argv=None):
                       "p90": res["launch_us_p90"], "avg": res["launch_us_avg"]},
         "push": {"us_median": res["push_us_median"], "gbps": res["push_gbps"],
                  "note": "full-step copy into the ring, once per full step (not in value)"},
+        "multi_target": multi,
         "parity_sample": par,
     }
     if not args.no_cpu_baseline:

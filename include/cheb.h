@@ -54,6 +54,8 @@ extern "C" {
 
 /* Largest history (K+1) the device kernels take. */
 #define CHEB_MAX_SLOTS 8
+/* Largest number of outputs (targets) one multi-target call produces. */
+#define CHEB_MAX_OUTPUTS 8
 /* Largest node count cheb_precompute_weights takes. */
 #define CHEB_MAX_NODES 64
 
@@ -118,6 +120,22 @@ CHEB_API int cheb_precompute_weights(const double *hist_t, int32_t n_hist,
  * CHEB_E_ALIGN, CHEB_E_NONFINITE, CHEB_E_HIP. */
 CHEB_API int cheb_combine(const void *const *src, int32_t n_src, const double *w,
                  void *out, int64_t numel, int32_t dtype, void *stream);
+
+/* Several targets from one pass over the sources:
+ *     out[m][i] = sum_k w[m * n_src + k] * src[k][i],  m < n_out.
+ * Every prediction between two full steps depends only on the same history
+ * (Section 3.3, forward application; Algorithm 1, the history changes only
+ * at full steps), so all of them can be formed while the history is read
+ * once: (n_src + n_out) x numel elements of traffic instead of
+ * n_out x (n_src + 1) x numel.
+ *   w    [n_out][n_src] host fp64, row-major.
+ *   out  [n_out] host array of device pointers, each 16-byte aligned, to
+ *        numel elements; outputs overlap neither each other nor a source.
+ * 1 <= n_out <= CHEB_MAX_OUTPUTS; other arguments as cheb_combine.
+ * Errors: as cheb_combine. */
+CHEB_API int cheb_combine_multi(const void *const *src, int32_t n_src, const double *w,
+                                int32_t n_out, void *const *out, int64_t numel,
+                                int32_t dtype, void *stream);
 
 /* ------------------------------------------------------------------------ */
 /* History cache: a ring of n entries in one caller-owned device arena.      */
@@ -211,6 +229,15 @@ CHEB_API int cheb_cache_slot_numel(const cheb_cache *c, int64_t *numel);
  * CHEB_E_NOTREADY, CHEB_E_ALIGN, CHEB_E_NONFINITE, CHEB_E_HIP. */
 CHEB_API int cheb_extrapolate(cheb_cache *c, const double *w, void *out, void *stream);
 
+/* The predictions for n_out targets from one pass over the history (see
+ * cheb_combine_multi): out[m] = sum_k w[m * n_slots + k] * H_k.
+ *   w    [n_out][n_slots] host fp64, rows aligned with cheb_cache_history.
+ *   out  [n_out] host array of device pointers, as cheb_extrapolate's out.
+ * Errors: as cheb_extrapolate, and CHEB_E_INVAL for n_out outside
+ * 1..CHEB_MAX_OUTPUTS. */
+CHEB_API int cheb_extrapolate_multi(cheb_cache *c, const double *w, int32_t n_out,
+                                    void *const *out, void *stream);
+
 /* Readiness check, weight row and prediction in one call: computes the fp64
  * coefficients of the held abscissae at `target_t` (as
  * cheb_precompute_weights) and runs cheb_extrapolate with them.  The weights
@@ -218,6 +245,14 @@ CHEB_API int cheb_extrapolate(cheb_cache *c, const double *w, void *out, void *s
  * Errors: those of cheb_precompute_weights and cheb_extrapolate. */
 CHEB_API int cheb_extrapolate_at(cheb_cache *c, double target_t, void *out,
                         void *stream, double *w_used);
+
+/* cheb_extrapolate_at for n_out targets in one pass over the history.
+ *   target_t  [n_out] host fp64.
+ *   out       [n_out] host array of device pointers.
+ *   w_used    [n_out][n_slots] host fp64 out, may be NULL.
+ * Errors: as cheb_extrapolate_at and cheb_extrapolate_multi. */
+CHEB_API int cheb_extrapolate_at_multi(cheb_cache *c, const double *target_t, int32_t n_out,
+                                       void *const *out, void *stream, double *w_used);
 
 /* ------------------------------------------------------------------------ */
 /* Launch shape (tuning).                                                    */

@@ -13,11 +13,12 @@ import numpy as np
 import torch
 
 from ._binding import (  # noqa: F401  (re-exported C entry points)
-    CHEB_BF16, CHEB_F32, CHEB_MAX_NODES, CHEB_MAX_SLOTS, ChebError,
+    CHEB_BF16, CHEB_F32, CHEB_MAX_NODES, CHEB_MAX_OUTPUTS, CHEB_MAX_SLOTS, ChebError,
     cheb_cache_begin_push, cheb_cache_commit, cheb_cache_create, cheb_cache_destroy,
     cheb_cache_entry, cheb_cache_history, cheb_cache_layout, cheb_cache_push,
     cheb_cache_reset, cheb_cache_segment_offset, cheb_cache_slot_numel, cheb_combine,
-    cheb_extrapolate, cheb_extrapolate_at, cheb_get_launch_config, cheb_last_error,
+    cheb_combine_multi, cheb_extrapolate, cheb_extrapolate_at, cheb_extrapolate_at_multi,
+    cheb_extrapolate_multi, cheb_get_launch_config, cheb_last_error,
     cheb_precompute_weights, cheb_set_launch_config, cheb_version,
 )
 from . import _binding
@@ -62,6 +63,22 @@ def combine(srcs: Sequence[torch.Tensor], w, out: torch.Tensor,
     cheb_combine([s.data_ptr() for s in srcs], w, out.data_ptr(), out.numel(), dt,
                  _stream_handle(stream))
     return out
+
+
+def combine_multi(srcs: Sequence[torch.Tensor], w, outs: Sequence[torch.Tensor],
+                  stream: Optional[torch.cuda.Stream] = None):
+    """outs[m] = sum_k w[m][k] * srcs[k], all outputs from one pass
+    (one launch of cheb_combine_multi)."""
+    if len(srcs) == 0 or len(outs) == 0:
+        raise ChebError(_binding.CHEB_E_INVAL, "no sources or no outputs")
+    dt = cheb_dtype(outs[0].dtype)
+    for i, t in enumerate(list(srcs) + list(outs)):
+        _check_device_tensor(t, f"tensor {i}")
+        if t.dtype != outs[0].dtype or t.numel() != outs[0].numel():
+            raise ChebError(_binding.CHEB_E_MISMATCH, f"tensor {i} differs in dtype or size")
+    cheb_combine_multi([s.data_ptr() for s in srcs], w, [o.data_ptr() for o in outs],
+                       outs[0].numel(), dt, _stream_handle(stream))
+    return outs
 
 
 def precompute_weights(hist_t, target_t) -> np.ndarray:
@@ -169,6 +186,25 @@ class ChebCache:
         cheb_extrapolate(self._h, w, out.data_ptr(), _stream_handle(stream))
         return out
 
+    def extrapolate_multi(self, w, outs: Optional[Sequence[torch.Tensor]] = None,
+                          stream: Optional[torch.cuda.Stream] = None):
+        w = np.asarray(w, dtype=np.float64).reshape(-1, self.n_slots)
+        outs = [self.new_output() for _ in range(w.shape[0])] if outs is None else list(outs)
+        for o in outs:
+            self._check_out(o)
+        cheb_extrapolate_multi(self._h, w, [o.data_ptr() for o in outs], _stream_handle(stream))
+        return outs
+
+    def extrapolate_at_multi(self, targets, outs: Optional[Sequence[torch.Tensor]] = None,
+                             stream: Optional[torch.cuda.Stream] = None):
+        targets = list(targets)
+        outs = [self.new_output() for _ in targets] if outs is None else list(outs)
+        for o in outs:
+            self._check_out(o)
+        w = cheb_extrapolate_at_multi(self._h, targets, [o.data_ptr() for o in outs],
+                                      _stream_handle(stream), n_slots=self.n_slots)
+        return outs, w
+
     def extrapolate_at(self, target_t: float, out: Optional[torch.Tensor] = None,
                        stream: Optional[torch.cuda.Stream] = None):
         out = self.new_output() if out is None else out
@@ -179,5 +215,5 @@ class ChebCache:
 
 
 __all__ = [n for n in dir() if n.startswith("cheb_")] + [
-    "ChebCache", "ChebError", "combine", "precompute_weights", "CHEB_BF16", "CHEB_F32",
-    "CHEB_MAX_SLOTS", "CHEB_MAX_NODES", "LIB_PATH"]
+    "ChebCache", "ChebError", "combine", "combine_multi", "precompute_weights", "CHEB_BF16",
+    "CHEB_F32", "CHEB_MAX_SLOTS", "CHEB_MAX_OUTPUTS", "CHEB_MAX_NODES", "LIB_PATH"]

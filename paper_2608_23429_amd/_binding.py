@@ -25,6 +25,7 @@ CHEB_E_NONFINITE = -8
 CHEB_BF16 = 0
 CHEB_F32 = 1
 CHEB_MAX_SLOTS = 8
+CHEB_MAX_OUTPUTS = 8
 CHEB_MAX_NODES = 64
 
 STATUS_NAMES = {
@@ -60,6 +61,8 @@ SIGNATURES = {
     "cheb_version": [],
     "cheb_precompute_weights": [_dp, ctypes.c_int32, _dp, ctypes.c_int32, _dp],
     "cheb_combine": [_vpp, ctypes.c_int32, _dp, _vp, ctypes.c_int64, ctypes.c_int32, _vp],
+    "cheb_combine_multi": [_vpp, ctypes.c_int32, _dp, ctypes.c_int32, _vpp, ctypes.c_int64,
+                           ctypes.c_int32, _vp],
     "cheb_cache_layout": [ctypes.c_int32, ctypes.c_int32, _i64p, ctypes.c_int32, _i64p,
                           _i64p, _szp, _szp],
     "cheb_cache_create": [ctypes.POINTER(_vp), ctypes.c_int32, ctypes.c_int32, _i64p,
@@ -75,6 +78,8 @@ SIGNATURES = {
     "cheb_cache_slot_numel": [_vp, _i64p],
     "cheb_extrapolate": [_vp, _dp, _vp, _vp],
     "cheb_extrapolate_at": [_vp, ctypes.c_double, _vp, _vp, _dp],
+    "cheb_extrapolate_multi": [_vp, _dp, ctypes.c_int32, _vpp, _vp],
+    "cheb_extrapolate_at_multi": [_vp, _dp, ctypes.c_int32, _vpp, _vp, _dp],
     "cheb_get_launch_config": [ctypes.POINTER(cheb_launch_config)],
     "cheb_set_launch_config": [ctypes.POINTER(cheb_launch_config)],
 }
@@ -136,6 +141,16 @@ def cheb_combine(src_ptrs, w, out_ptr, numel, dtype, stream=0):
     arr = _voidp_array(src_ptrs)
     _check(LIB.cheb_combine(arr, len(src_ptrs), _dptr(w), ctypes.c_void_p(int(out_ptr)),
                             int(numel), int(dtype), ctypes.c_void_p(int(stream))))
+
+
+def cheb_combine_multi(src_ptrs, w, out_ptrs, numel, dtype, stream=0):
+    """w: [n_out, n_src] fp64."""
+    w = _f64(w)
+    n_out = len(out_ptrs)
+    w = w.reshape(n_out, len(src_ptrs))
+    _check(LIB.cheb_combine_multi(_voidp_array(src_ptrs), len(src_ptrs), _dptr(w), n_out,
+                                  _voidp_array(out_ptrs), int(numel), int(dtype),
+                                  ctypes.c_void_p(int(stream))))
 
 
 def cheb_cache_layout(n_slots, dtype, seg_numel):
@@ -219,6 +234,23 @@ def cheb_extrapolate_at(handle, target_t, out_ptr, stream=0, n_slots=CHEB_MAX_SL
     _check(LIB.cheb_extrapolate_at(handle, float(target_t), ctypes.c_void_p(int(out_ptr)),
                                    ctypes.c_void_p(int(stream)), _dptr(w)))
     return w[:n_slots].copy()
+
+
+def cheb_extrapolate_multi(handle, w, out_ptrs, stream=0):
+    """w: [n_out, n_slots] fp64, rows aligned with cheb_cache_history."""
+    w = _f64(w).reshape(len(out_ptrs), -1)
+    _check(LIB.cheb_extrapolate_multi(handle, _dptr(w), len(out_ptrs), _voidp_array(out_ptrs),
+                                      ctypes.c_void_p(int(stream))))
+
+
+def cheb_extrapolate_at_multi(handle, targets, out_ptrs, stream=0, n_slots=CHEB_MAX_SLOTS):
+    t = _f64(targets).reshape(-1)
+    if t.size != len(out_ptrs):
+        raise ChebError(CHEB_E_INVAL, "one output per target")
+    w = np.zeros((CHEB_MAX_OUTPUTS, CHEB_MAX_SLOTS), dtype=np.float64)
+    _check(LIB.cheb_extrapolate_at_multi(handle, _dptr(t), t.size, _voidp_array(out_ptrs),
+                                         ctypes.c_void_p(int(stream)), _dptr(w)))
+    return w.reshape(-1)[:t.size * n_slots].reshape(t.size, n_slots).copy()
 
 
 def cheb_get_launch_config():

@@ -176,29 +176,46 @@ int cheb_precompute_weights(const double *hist_t, int32_t n_hist, const double *
   return ok();
 }
 
-int cheb_combine(const void *const *src, int32_t n_src, const double *w, void *out,
-                 int64_t numel, int32_t dtype, void *stream) {
+int cheb_combine_multi(const void *const *src, int32_t n_src, const double *w, int32_t n_out,
+                       void *const *out, int64_t numel, int32_t dtype, void *stream) {
   if (!valid_dtype(dtype)) return fail(CHEB_E_DTYPE, "unknown dtype %d", dtype);
   if (n_src < 1 || n_src > CHEB_MAX_SLOTS)
     return fail(CHEB_E_INVAL, "n_src %d outside 1..%d", n_src, CHEB_MAX_SLOTS);
-  if (!src || !w) return fail(CHEB_E_INVAL, "src or w is NULL");
+  if (n_out < 1 || n_out > CHEB_MAX_OUTPUTS)
+    return fail(CHEB_E_INVAL, "n_out %d outside 1..%d", n_out, CHEB_MAX_OUTPUTS);
+  if (!src || !w || !out) return fail(CHEB_E_INVAL, "src, w or out is NULL");
   if (numel < 0) return fail(CHEB_E_INVAL, "numel is negative");
   if (numel / elems_per_vec(dtype) >= kMaxVecs)
     return fail(CHEB_E_INVAL, "numel %lld too large for one launch", (long long)numel);
+  for (int m = 0; m < n_out * n_src; ++m)
+    if (!isfinite(w[m])) return fail(CHEB_E_NONFINITE, "weight %d is not finite", m);
   if (numel == 0) return ok();
-  if (!out) return fail(CHEB_E_INVAL, "out is NULL");
-  if (!aligned16(out)) return fail(CHEB_E_ALIGN, "out is not 16-byte aligned");
   const uintptr_t bytes = uintptr_t(numel) * elem_bytes(dtype);
-  const uintptr_t o0 = reinterpret_cast<uintptr_t>(out);
+  auto overlap = [bytes](const void *a, const void *b) {
+    const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+    return x < y + bytes && y < x + bytes;
+  };
   for (int k = 0; k < n_src; ++k) {
     if (!src[k]) return fail(CHEB_E_INVAL, "src[%d] is NULL", k);
     if (!aligned16(src[k])) return fail(CHEB_E_ALIGN, "src[%d] is not 16-byte aligned", k);
-    if (!isfinite(w[k])) return fail(CHEB_E_NONFINITE, "w[%d] is not finite", k);
-    const uintptr_t s0 = reinterpret_cast<uintptr_t>(src[k]);
-    if (s0 < o0 + bytes && o0 < s0 + bytes)
-      return fail(CHEB_E_INVAL, "out overlaps src[%d]", k);
   }
-  return launch_combine(dtype, src, n_src, w, out, numel, static_cast<hipStream_t>(stream));
+  for (int m = 0; m < n_out; ++m) {
+    if (!out[m]) return fail(CHEB_E_INVAL, "out[%d] is NULL", m);
+    if (!aligned16(out[m])) return fail(CHEB_E_ALIGN, "out[%d] is not 16-byte aligned", m);
+    for (int k = 0; k < n_src; ++k)
+      if (overlap(out[m], src[k])) return fail(CHEB_E_INVAL, "out[%d] overlaps src[%d]", m, k);
+    for (int j = 0; j < m; ++j)
+      if (overlap(out[m], out[j])) return fail(CHEB_E_INVAL, "out[%d] overlaps out[%d]", m, j);
+  }
+  return launch_combine(dtype, src, n_src, w, n_out, out, numel,
+                        static_cast<hipStream_t>(stream));
+}
+
+int cheb_combine(const void *const *src, int32_t n_src, const double *w, void *out,
+                 int64_t numel, int32_t dtype, void *stream) {
+  void *outs[1] = {out};
+  if (numel > 0 && !out) return fail(CHEB_E_INVAL, "out is NULL");
+  return cheb_combine_multi(src, n_src, w, 1, outs, numel, dtype, stream);
 }
 
 }  // extern "C"

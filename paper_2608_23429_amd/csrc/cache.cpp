@@ -223,37 +223,60 @@ int cheb_cache_slot_numel(const cheb_cache *c, int64_t *numel) {
   return ok();
 }
 
-int cheb_extrapolate(cheb_cache *c, const double *w, void *out, void *stream) {
-  if (!c || !w) return fail(CHEB_E_INVAL, "cache or w is NULL");
+int cheb_extrapolate_multi(cheb_cache *c, const double *w, int32_t n_out, void *const *out,
+                           void *stream) {
+  if (!c || !w || !out) return fail(CHEB_E_INVAL, "cache, w or out is NULL");
   if (c->push_open) return fail(CHEB_E_NOTREADY, "a fused push is open");
   if (c->count < c->n_slots)
     return fail(CHEB_E_NOTREADY, "history holds %d of %d entries", c->count, c->n_slots);
+  if (n_out < 1 || n_out > CHEB_MAX_OUTPUTS)
+    return fail(CHEB_E_INVAL, "n_out %d outside 1..%d", n_out, CHEB_MAX_OUTPUTS);
   const void *src[CHEB_MAX_SLOTS];
   for (int32_t a = 0; a < c->n_slots; ++a) src[a] = c->slot_ptr(c->slot_of_age(a));
   if (c->slot_numel > 0) {
-    if (!out) return fail(CHEB_E_INVAL, "out is NULL");
-    const uintptr_t o0 = reinterpret_cast<uintptr_t>(out);
     const uintptr_t a0 = reinterpret_cast<uintptr_t>(c->arena);
     const uintptr_t ob = uintptr_t(c->slot_numel) * uintptr_t(elem_bytes(c->dtype));
-    if (o0 < a0 + c->arena_bytes && a0 < o0 + ob)
-      return fail(CHEB_E_INVAL, "out overlaps the cache arena");
+    for (int32_t m = 0; m < n_out; ++m) {
+      if (!out[m]) return fail(CHEB_E_INVAL, "out[%d] is NULL", m);
+      const uintptr_t o0 = reinterpret_cast<uintptr_t>(out[m]);
+      if (o0 < a0 + c->arena_bytes && a0 < o0 + ob)
+        return fail(CHEB_E_INVAL, "out[%d] overlaps the cache arena", m);
+    }
   }
-  return cheb_combine(src, c->n_slots, w, out, c->slot_numel, c->dtype, stream);
+  return cheb_combine_multi(src, c->n_slots, w, n_out, out, c->slot_numel, c->dtype, stream);
+}
+
+int cheb_extrapolate(cheb_cache *c, const double *w, void *out, void *stream) {
+  void *outs[1] = {out};
+  if (!out && c && c->slot_numel > 0) return fail(CHEB_E_INVAL, "out is NULL");
+  return cheb_extrapolate_multi(c, w, 1, outs, stream);
+}
+
+int cheb_extrapolate_at_multi(cheb_cache *c, const double *target_t, int32_t n_out,
+                              void *const *out, void *stream, double *w_used) {
+  if (!c || !target_t) return fail(CHEB_E_INVAL, "cache or target_t is NULL");
+  if (c->push_open) return fail(CHEB_E_NOTREADY, "a fused push is open");
+  if (c->count < c->n_slots)
+    return fail(CHEB_E_NOTREADY, "history holds %d of %d entries", c->count, c->n_slots);
+  if (n_out < 1 || n_out > CHEB_MAX_OUTPUTS)
+    return fail(CHEB_E_INVAL, "n_out %d outside 1..%d", n_out, CHEB_MAX_OUTPUTS);
+  double t[CHEB_MAX_SLOTS], w[CHEB_MAX_OUTPUTS * CHEB_MAX_SLOTS];
+  for (int32_t a = 0; a < c->n_slots; ++a) t[a] = c->slot_t[c->slot_of_age(a)];
+  for (int32_t m = 0; m < n_out; ++m) {
+    int rc = weights_row(t, c->n_slots, target_t[m], w + m * c->n_slots);
+    if (rc != CHEB_OK) return rc;
+  }
+  int rc = cheb_extrapolate_multi(c, w, n_out, out, stream);
+  if (rc == CHEB_OK && w_used)
+    memcpy(w_used, w, sizeof(double) * size_t(n_out) * size_t(c->n_slots));
+  return rc;
 }
 
 int cheb_extrapolate_at(cheb_cache *c, double target_t, void *out, void *stream,
                         double *w_used) {
-  if (!c) return fail(CHEB_E_INVAL, "cache is NULL");
-  if (c->push_open) return fail(CHEB_E_NOTREADY, "a fused push is open");
-  if (c->count < c->n_slots)
-    return fail(CHEB_E_NOTREADY, "history holds %d of %d entries", c->count, c->n_slots);
-  double t[CHEB_MAX_SLOTS], w[CHEB_MAX_SLOTS];
-  for (int32_t a = 0; a < c->n_slots; ++a) t[a] = c->slot_t[c->slot_of_age(a)];
-  int rc = weights_row(t, c->n_slots, target_t, w);
-  if (rc != CHEB_OK) return rc;
-  rc = cheb_extrapolate(c, w, out, stream);
-  if (rc == CHEB_OK && w_used) memcpy(w_used, w, sizeof(double) * size_t(c->n_slots));
-  return rc;
+  void *outs[1] = {out};
+  if (!out && c && c->slot_numel > 0) return fail(CHEB_E_INVAL, "out is NULL");
+  return cheb_extrapolate_at_multi(c, &target_t, 1, outs, stream, w_used);
 }
 
 }  // extern "C"

@@ -35,10 +35,12 @@ int device_cus(int *cus);
 // CHEB_OK or an error code with the message set.
 int weights_row(const double *x, int n, double target, double *w);
 
-// out[i] = sum_k w[k] * src[k][i], i < numel.  Arguments already validated:
-// 1 <= n <= CHEB_MAX_SLOTS, pointers 16-byte aligned, numel below the limit.
-int launch_combine(int dtype, const void *const *src, int n, const double *w,
-                   void *out, int64_t numel, hipStream_t stream);
+// out[m][i] = sum_k w[m * n + k] * src[k][i], i < numel, m < n_out, in one
+// launch.  Arguments already validated: 1 <= n <= CHEB_MAX_SLOTS,
+// 1 <= n_out <= CHEB_MAX_OUTPUTS, pointers 16-byte aligned, numel below the
+// limit.
+int launch_combine(int dtype, const void *const *src, int n, const double *w, int n_out,
+                   void *const *out, int64_t numel, hipStream_t stream);
 
 // Segment copy into one slot; zero-fills each segment's padding up to the
 // next 16-byte boundary.

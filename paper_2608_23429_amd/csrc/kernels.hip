@@ -2,7 +2,8 @@
 //
 // 1. The skipped-step prediction (paper, Section 3.3, forward application
 //    equation; Algorithm 1, extrapolation branch): out = sum_k w_k H_k over
-//    the flattened feature cache.  Pure streaming work: (n+1) x 16 bytes of
+//    the flattened feature cache, for one target or for several targets
+//    at once (all of them depend on the same history).  Pure streaming work: (n+1) x 16 bytes of
 //    HBM traffic per 16-byte output vector and 2n flops per element, far
 //    below the fp32 ridge point, so the kernel is laid out for bandwidth:
 //    128-bit coalesced loads (a wave covers 1 KiB contiguous per load
@@ -43,12 +44,13 @@ __device__ __forceinline__ void store16(u32x4 *p, u32x4 v) {
   else *p = v;
 }
 
-// History pointers (oldest to newest) and weights, passed by value as kernel
-// arguments.
-template <int NS, typename W>
+// History pointers (oldest to newest), output pointers and one weight row
+// per output, passed by value as kernel arguments (they land in SGPRs).
+template <int NS, int NO, typename W>
 struct Hist {
   const u32x4 *p[NS];
-  W w[NS];
+  u32x4 *o[NO];
+  W w[NO][NS];
 };
 
 // Ragged end of a stateless combination: `count` (< elements per vector)
@@ -145,10 +147,11 @@ struct F32Op {
 // lane t handles vectors t, t + BLK, ..., so every load instruction of a
 // wave reads 64 consecutive 16-byte vectors (1 KiB).  A scheduling barrier
 // keeps all NS x U loads of a thread ahead of its arithmetic, so each wave
-// has its whole working set in flight before it waits.
-template <class Op, int NS, int BLK, int U, bool NT>
-__global__ __launch_bounds__(BLK) void combine_kernel(Hist<NS, typename Op::W> h,
-                                                      u32x4 *__restrict__ out,
+// has its whole working set in flight before it waits.  With NO > 1 the same
+// loaded history feeds NO weight rows and NO outputs: every skipped step
+// between two full steps is predicted in one pass over the history.
+template <class Op, int NS, int NO, int BLK, int U, bool NT>
+__global__ __launch_bounds__(BLK) void combine_kernel(Hist<NS, NO, typename Op::W> h,
                                                       uint32_t n_vec, uint32_t n_tiles,
                                                       Tail tail) {
   for (uint32_t tile = blockIdx.x; tile < n_tiles; tile += gridDim.x) {
@@ -161,7 +164,10 @@ __global__ __launch_bounds__(BLK) void combine_kernel(Hist<NS, typename Op::W> h
         for (int k = 0; k < NS; ++k) v[u][k] = load16<NT>(h.p[k] + base + u * BLK);
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int u = 0; u < U; ++u) store16<NT>(out + base + u * BLK, Op::template vec<NS>(v[u], h.w));
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int m = 0; m < NO; ++m)
+          store16<NT>(h.o[m] + base + u * BLK, Op::template vec<NS>(v[u], h.w[m]));
     } else {
 #pragma unroll
       for (int u = 0; u < U; ++u) {
@@ -170,7 +176,8 @@ __global__ __launch_bounds__(BLK) void combine_kernel(Hist<NS, typename Op::W> h
           u32x4 v[NS];
 #pragma unroll
           for (int k = 0; k < NS; ++k) v[k] = load16<NT>(h.p[k] + i);
-          store16<NT>(out + i, Op::template vec<NS>(v, h.w));
+#pragma unroll
+          for (int m = 0; m < NO; ++m) store16<NT>(h.o[m] + i, Op::template vec<NS>(v, h.w[m]));
         }
       }
     }
@@ -181,64 +188,97 @@ __global__ __launch_bounds__(BLK) void combine_kernel(Hist<NS, typename Op::W> h
 #pragma unroll
     for (int k = 0; k < NS; ++k) p[k] = reinterpret_cast<const E *>(h.p[k]);
     const uint64_t i = tail.first + threadIdx.x;
-    reinterpret_cast<E *>(out)[i] = Op::template scalar<NS>(p, h.w, i);
+#pragma unroll
+    for (int m = 0; m < NO; ++m)
+      reinterpret_cast<E *>(h.o[m])[i] = Op::template scalar<NS>(p, h.w[m], i);
   }
 }
 
-template <class Op, int NS, int BLK, int U, bool NT>
-hipError_t launch_shape_ns(const Hist<NS, typename Op::W> &h, u32x4 *out, uint32_t n_vec,
-                           Tail tail, int blocks_per_cu, int cus, hipStream_t s) {
+template <class Op, int NS, int NO, int BLK, int U, bool NT>
+hipError_t launch_shape(const Hist<NS, NO, typename Op::W> &h, uint32_t n_vec, Tail tail,
+                        int blocks_per_cu, int cus, hipStream_t s) {
   const uint32_t per_tile = uint32_t(BLK * U);
   const uint32_t n_tiles = (n_vec + per_tile - 1) / per_tile;
   uint32_t grid = std::max<uint32_t>(n_tiles, 1u);
   if (blocks_per_cu > 0) grid = std::min<uint32_t>(grid, uint32_t(blocks_per_cu) * uint32_t(cus));
-  hipLaunchKernelGGL((combine_kernel<Op, NS, BLK, U, NT>), dim3(grid), dim3(BLK), 0, s, h, out,
+  hipLaunchKernelGGL((combine_kernel<Op, NS, NO, BLK, U, NT>), dim3(grid), dim3(BLK), 0, s, h,
                      n_vec, n_tiles, tail);
   return hipGetLastError();
 }
 
+// Single output: every launch shape of the tuning interface.
 template <class Op, int NS, bool NT>
-hipError_t launch_nt(const Hist<NS, typename Op::W> &h, u32x4 *out, uint32_t n_vec, Tail tail,
-                     const cheb_launch_config &cfg, int cus, hipStream_t s) {
+hipError_t launch_one(const Hist<NS, 1, typename Op::W> &h, uint32_t n_vec, Tail tail,
+                      const cheb_launch_config &cfg, int cus, hipStream_t s) {
   const int b = cfg.block, u = cfg.unroll, g = cfg.blocks_per_cu;
-  if (b == 1024) return launch_shape_ns<Op, NS, 1024, 1, NT>(h, out, n_vec, tail, g, cus, s);
+  if (b == 1024) return launch_shape<Op, NS, 1, 1024, 1, NT>(h, n_vec, tail, g, cus, s);
   if (b == 512) {
-    if (u == 1) return launch_shape_ns<Op, NS, 512, 1, NT>(h, out, n_vec, tail, g, cus, s);
-    return launch_shape_ns<Op, NS, 512, 2, NT>(h, out, n_vec, tail, g, cus, s);
+    if (u == 1) return launch_shape<Op, NS, 1, 512, 1, NT>(h, n_vec, tail, g, cus, s);
+    return launch_shape<Op, NS, 1, 512, 2, NT>(h, n_vec, tail, g, cus, s);
   }
-  if (u == 1) return launch_shape_ns<Op, NS, 256, 1, NT>(h, out, n_vec, tail, g, cus, s);
-  if (u == 2) return launch_shape_ns<Op, NS, 256, 2, NT>(h, out, n_vec, tail, g, cus, s);
-  return launch_shape_ns<Op, NS, 256, 4, NT>(h, out, n_vec, tail, g, cus, s);
+  if (u == 1) return launch_shape<Op, NS, 1, 256, 1, NT>(h, n_vec, tail, g, cus, s);
+  if (u == 2) return launch_shape<Op, NS, 1, 256, 2, NT>(h, n_vec, tail, g, cus, s);
+  return launch_shape<Op, NS, 1, 256, 4, NT>(h, n_vec, tail, g, cus, s);
 }
 
-template <class Op, int NS>
-hipError_t launch_ns(const void *const *src, const double *w, void *out, int64_t numel,
-                     const cheb_launch_config &cfg, int cus, hipStream_t s) {
+// Several outputs: one shape (1024 threads, one vector per lane, the
+// non-temporal hint as configured, grid covering the range), which keeps the
+// number of kernel instances bounded.
+template <class Op, int NS, int NO>
+hipError_t launch_many(const Hist<NS, NO, typename Op::W> &h, uint32_t n_vec, Tail tail,
+                       const cheb_launch_config &cfg, int cus, hipStream_t s) {
+  return cfg.nontemporal ? launch_shape<Op, NS, NO, 1024, 1, true>(h, n_vec, tail, 0, cus, s)
+                         : launch_shape<Op, NS, NO, 1024, 1, false>(h, n_vec, tail, 0, cus, s);
+}
+
+template <class Op, int NS, int NO>
+hipError_t launch_ns_no(const void *const *src, const double *w, void *const *out,
+                        int64_t numel, const cheb_launch_config &cfg, int cus, hipStream_t s) {
   constexpr int kVec = 16 / int(sizeof(typename Op::E));
-  Hist<NS, typename Op::W> h;
-  for (int k = 0; k < NS; ++k) {
-    h.p[k] = static_cast<const u32x4 *>(src[k]);
-    h.w[k] = static_cast<typename Op::W>(w[k]);
+  Hist<NS, NO, typename Op::W> h;
+  for (int k = 0; k < NS; ++k) h.p[k] = static_cast<const u32x4 *>(src[k]);
+  for (int m = 0; m < NO; ++m) {
+    h.o[m] = static_cast<u32x4 *>(out[m]);
+    for (int k = 0; k < NS; ++k) h.w[m][k] = static_cast<typename Op::W>(w[m * NS + k]);
   }
   const uint32_t n_vec = uint32_t(numel / kVec);
   Tail tail{uint32_t(numel % kVec), uint64_t(numel / kVec) * kVec};
-  u32x4 *o = static_cast<u32x4 *>(out);
-  return cfg.nontemporal ? launch_nt<Op, NS, true>(h, o, n_vec, tail, cfg, cus, s)
-                         : launch_nt<Op, NS, false>(h, o, n_vec, tail, cfg, cus, s);
+  if constexpr (NO == 1) {
+    return cfg.nontemporal ? launch_one<Op, NS, true>(h, n_vec, tail, cfg, cus, s)
+                           : launch_one<Op, NS, false>(h, n_vec, tail, cfg, cus, s);
+  } else {
+    return launch_many<Op, NS, NO>(h, n_vec, tail, cfg, cus, s);
+  }
+}
+
+template <class Op, int NS>
+hipError_t launch_ns(const void *const *src, const double *w, int n_out, void *const *out,
+                     int64_t numel, const cheb_launch_config &cfg, int cus, hipStream_t s) {
+  switch (n_out) {
+    case 1: return launch_ns_no<Op, NS, 1>(src, w, out, numel, cfg, cus, s);
+    case 2: return launch_ns_no<Op, NS, 2>(src, w, out, numel, cfg, cus, s);
+    case 3: return launch_ns_no<Op, NS, 3>(src, w, out, numel, cfg, cus, s);
+    case 4: return launch_ns_no<Op, NS, 4>(src, w, out, numel, cfg, cus, s);
+    case 5: return launch_ns_no<Op, NS, 5>(src, w, out, numel, cfg, cus, s);
+    case 6: return launch_ns_no<Op, NS, 6>(src, w, out, numel, cfg, cus, s);
+    case 7: return launch_ns_no<Op, NS, 7>(src, w, out, numel, cfg, cus, s);
+    default: return launch_ns_no<Op, NS, 8>(src, w, out, numel, cfg, cus, s);
+  }
 }
 
 template <class Op>
-hipError_t launch_op(const void *const *src, int n, const double *w, void *out, int64_t numel,
-                     const cheb_launch_config &cfg, int cus, hipStream_t s) {
+hipError_t launch_op(const void *const *src, int n, const double *w, int n_out,
+                     void *const *out, int64_t numel, const cheb_launch_config &cfg, int cus,
+                     hipStream_t s) {
   switch (n) {
-    case 1: return launch_ns<Op, 1>(src, w, out, numel, cfg, cus, s);
-    case 2: return launch_ns<Op, 2>(src, w, out, numel, cfg, cus, s);
-    case 3: return launch_ns<Op, 3>(src, w, out, numel, cfg, cus, s);
-    case 4: return launch_ns<Op, 4>(src, w, out, numel, cfg, cus, s);
-    case 5: return launch_ns<Op, 5>(src, w, out, numel, cfg, cus, s);
-    case 6: return launch_ns<Op, 6>(src, w, out, numel, cfg, cus, s);
-    case 7: return launch_ns<Op, 7>(src, w, out, numel, cfg, cus, s);
-    default: return launch_ns<Op, 8>(src, w, out, numel, cfg, cus, s);
+    case 1: return launch_ns<Op, 1>(src, w, n_out, out, numel, cfg, cus, s);
+    case 2: return launch_ns<Op, 2>(src, w, n_out, out, numel, cfg, cus, s);
+    case 3: return launch_ns<Op, 3>(src, w, n_out, out, numel, cfg, cus, s);
+    case 4: return launch_ns<Op, 4>(src, w, n_out, out, numel, cfg, cus, s);
+    case 5: return launch_ns<Op, 5>(src, w, n_out, out, numel, cfg, cus, s);
+    case 6: return launch_ns<Op, 6>(src, w, n_out, out, numel, cfg, cus, s);
+    case 7: return launch_ns<Op, 7>(src, w, n_out, out, numel, cfg, cus, s);
+    default: return launch_ns<Op, 8>(src, w, n_out, out, numel, cfg, cus, s);
   }
 }
 
@@ -297,16 +337,16 @@ __global__ __launch_bounds__(kBlock) void gather_kernel(GatherArgs a, char *__re
 
 }  // namespace
 
-int launch_combine(int dtype, const void *const *src, int n, const double *w, void *out,
-                   int64_t numel, hipStream_t stream) {
+int launch_combine(int dtype, const void *const *src, int n, const double *w, int n_out,
+                   void *const *out, int64_t numel, hipStream_t stream) {
   if (numel == 0) return ok();
   int cus = 0;
   int rc = device_cus(&cus);
   if (rc != CHEB_OK) return rc;
   const cheb_launch_config cfg = launch_shape();
   hipError_t e = dtype == CHEB_BF16
-                     ? launch_op<Bf16Op>(src, n, w, out, numel, cfg, cus, stream)
-                     : launch_op<F32Op>(src, n, w, out, numel, cfg, cus, stream);
+                     ? launch_op<Bf16Op>(src, n, w, n_out, out, numel, cfg, cus, stream)
+                     : launch_op<F32Op>(src, n, w, n_out, out, numel, cfg, cus, stream);
   if (e != hipSuccess) return fail(CHEB_E_HIP, "combine launch failed: %s", hipGetErrorString(e));
   return ok();
 }

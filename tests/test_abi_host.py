@@ -302,3 +302,44 @@ def test_launch_config_roundtrip_and_validation():
         assert cheb.cheb_get_launch_config()["block"] == 256     # unchanged by failures
     finally:
         cheb.cheb_set_launch_config(**old)
+
+
+def test_combine_multi_validation_before_launch():
+    a, b = FAKE_ARENA, FAKE_ARENA + (1 << 30)
+    o1, o2 = FAKE_ARENA + (2 << 30), FAKE_ARENA + (3 << 30)
+    w2 = [[0.5, 0.5], [-1.0, 2.0]]
+    cases = [
+        (([a, b], [[0.5, 0.5]] * 9, [o1 + (k << 28) for k in range(9)], 100, 0), B.CHEB_E_INVAL),
+        (([a, b], w2, [o1, o1 + 64], 100, 0), B.CHEB_E_INVAL),         # outputs overlap
+        (([a, b], w2, [o1, b + 32], 100, 0), B.CHEB_E_INVAL),          # output overlaps a source
+        (([a, b], w2, [o1, o2 + 8], 100, 0), B.CHEB_E_ALIGN),
+        (([a, b], [[0.5, 0.5], [np.inf, 0.0]], [o1, o2], 100, 0), B.CHEB_E_NONFINITE),
+        (([a, b], w2, [o1, 0], 100, 0), B.CHEB_E_INVAL),
+        (([a, b], w2, [o1, o2], 100, 9), B.CHEB_E_DTYPE),
+    ]
+    for args, code in cases:
+        with pytest.raises(cheb.ChebError) as e:
+            cheb.cheb_combine_multi(*args)
+        assert e.value.code == code, (args, e.value)
+    cheb.cheb_combine_multi([a, b], w2, [o1, o2], 0, 0)       # empty: no work
+
+
+def test_extrapolate_multi_not_ready_and_limits():
+    h, lay = _fake_cache(n_slots=2)
+    outs = [FAKE_ARENA + (4 + k) * lay["arena_bytes"] for k in range(3)]
+    with pytest.raises(cheb.ChebError) as e:
+        cheb.cheb_extrapolate_at_multi(h, [5.0, 6.0, 7.0], outs)
+    assert e.value.code == B.CHEB_E_NOTREADY
+    for t in [1.0, 2.0]:
+        cheb.cheb_cache_begin_push(h)
+        cheb.cheb_cache_commit(h, t)
+    with pytest.raises(cheb.ChebError) as e:
+        cheb.cheb_extrapolate_multi(h, np.zeros((9, 2)), [outs[0]] * 9)
+    assert e.value.code == B.CHEB_E_INVAL
+    with pytest.raises(cheb.ChebError) as e:         # output inside the arena
+        cheb.cheb_extrapolate_multi(h, np.ones((1, 2)), [FAKE_ARENA + 256])
+    assert e.value.code == B.CHEB_E_INVAL
+    with pytest.raises(cheb.ChebError) as e:         # duplicate of a held node is fine, NaN is not
+        cheb.cheb_extrapolate_at_multi(h, [float("nan")], outs[:1])
+    assert e.value.code == B.CHEB_E_NONFINITE
+    cheb.cheb_cache_destroy(h)
