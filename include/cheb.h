@@ -68,7 +68,8 @@ typedef enum cheb_status {
   CHEB_E_ALIGN = -5,     /* device pointer not aligned as documented */
   CHEB_E_HIP = -6,       /* the HIP runtime reported an error */
   CHEB_E_MISMATCH = -7,  /* sizes disagree (arena too small, ...) */
-  CHEB_E_NONFINITE = -8  /* NaN or infinite abscissa or weight */
+  CHEB_E_NONFINITE = -8, /* NaN or infinite abscissa or weight */
+  CHEB_E_IO = -9         /* table file cannot be read or written, or is malformed */
 } cheb_status;
 
 typedef enum cheb_dtype { CHEB_BF16 = 0, CHEB_F32 = 1 } cheb_dtype;
@@ -214,6 +215,9 @@ CHEB_API int cheb_cache_entry(const cheb_cache *c, int32_t idx, void **slot_base
 CHEB_API int cheb_cache_segment_offset(const cheb_cache *c, int32_t seg,
                               int64_t *elem_offset);
 
+/* Storage type (cheb_dtype) of the cache. */
+CHEB_API int cheb_cache_dtype(const cheb_cache *c, int32_t *dtype);
+
 /* Elements of one slot (= elements an output buffer must hold). */
 CHEB_API int cheb_cache_slot_numel(const cheb_cache *c, int64_t *numel);
 
@@ -253,6 +257,72 @@ CHEB_API int cheb_extrapolate_at(cheb_cache *c, double target_t, void *out,
  * Errors: as cheb_extrapolate_at and cheb_extrapolate_multi. */
 CHEB_API int cheb_extrapolate_at_multi(cheb_cache *c, const double *target_t, int32_t n_out,
                                        void *const *out, void *stream, double *w_used);
+
+/* ------------------------------------------------------------------------ */
+/* Offline stage: schedule and weight table.                                 */
+/* ------------------------------------------------------------------------ */
+
+/* The full-computation schedule F of Section 3.3 (weight precomputation):
+ * step s of 0..T-1 runs the full network when s < s0, or s > T-1-s1, or r
+ * divides s - s0.  is_full [T] host out: 1 for s in F, else 0.
+ * 1 <= T <= 2^20, s0 >= 0, s1 >= 0, r >= 1.  Errors: CHEB_E_INVAL. */
+CHEB_API int cheb_schedule(int32_t T, int32_t s0, int32_t s1, int32_t r, uint8_t *is_full);
+
+/* What a skipped step does when fewer than n_hist full steps precede it
+ * (the paper requires |H| = n and leaves this case open). */
+enum { CHEB_SHORT_FULL = 0,   /* run the full network instead (it joins H) */
+       CHEB_SHORT_LOWER = 1 }; /* predict from the entries held (lower degree) */
+
+/* The weight table of the offline stage (Algorithm 1, offline stage;
+ * Section 3.3): for every step outside F (and the policy's extra full
+ * steps), the steps of the history it predicts from (the n_hist most recent
+ * steps that ran the network, or fewer under CHEB_SHORT_LOWER) and its fp64
+ * coefficients over their abscissae at the step's own abscissa
+ * (cheb_precompute_weights).  Host-only object, library-owned. */
+typedef struct cheb_table cheb_table;
+
+/* Builds the table.  abscissa [T] host fp64: the value each step is
+ * interpolated in (timestep t or sigma), finite; steps that share a
+ * history must have distinct abscissae.  1 <= n_hist <= CHEB_MAX_SLOTS.
+ * Errors: CHEB_E_INVAL, CHEB_E_NONFINITE, CHEB_E_DUPNODE. */
+CHEB_API int cheb_table_build(cheb_table **out, int32_t T, int32_t s0, int32_t s1, int32_t r,
+                              int32_t n_hist, const double *abscissa, int32_t policy);
+
+/* Frees the table.  NULL is accepted. */
+CHEB_API int cheb_table_destroy(cheb_table *t);
+
+/* Sizes of a table; every output may be NULL.  n_full counts the steps that
+ * run the network (the schedule's plus the policy's). */
+CHEB_API int cheb_table_info(const cheb_table *t, int32_t *T, int32_t *n_hist,
+                             int32_t *policy, int32_t *n_full);
+
+/* Row of one step: *predicted (1 predicted, 0 full), *n_used (entries the
+ * prediction uses), node_steps [n_hist] (their steps, oldest to newest) and
+ * w [n_hist] (their coefficients); node_steps and w may be NULL.
+ * Errors: CHEB_E_INVAL. */
+CHEB_API int cheb_table_step(const cheb_table *t, int32_t step, int32_t *predicted,
+                             int32_t *n_used, int32_t *node_steps, double *w);
+
+/* Writes the table as text (hexadecimal floats, so it reads back bit for
+ * bit) to `path`: the "prepackaged" tables of Section 3.3.  Errors:
+ * CHEB_E_INVAL, CHEB_E_IO. */
+CHEB_API int cheb_table_save(const cheb_table *t, const char *path);
+
+/* Reads a table written by cheb_table_save.  Rows are taken as stored,
+ * after structural checks (step order, node steps before the step and
+ * increasing, finite values).  Errors: CHEB_E_INVAL, CHEB_E_IO. */
+CHEB_API int cheb_table_load(cheb_table **out, const char *path);
+
+/* The online stage driven by a table (Algorithm 1, extrapolation branch;
+ * Section 3.3, forward application): predicts steps first_step ..
+ * first_step + n_steps - 1, which must all be predicted steps sharing one
+ * history, from one pass over that history.  The newest n_used entries of
+ * the cache must hold exactly the abscissae of the row's nodes (the row
+ * matches the ring), else CHEB_E_MISMATCH.  out [n_steps] device pointers as
+ * in cheb_extrapolate_multi.  Errors: CHEB_E_INVAL, CHEB_E_MISMATCH,
+ * CHEB_E_NOTREADY, and those of cheb_extrapolate_multi. */
+CHEB_API int cheb_extrapolate_steps(cheb_cache *c, const cheb_table *t, int32_t first_step,
+                                    int32_t n_steps, void *const *out, void *stream);
 
 /* ------------------------------------------------------------------------ */
 /* Launch shape (tuning).                                                    */

@@ -77,6 +77,9 @@ def bind(path):
     L.oracle_extrapolate_f64.restype = None
     L.oracle_full_schedule.argtypes = [ctypes.c_int] * 4 + [
         ctypes.POINTER(ctypes.c_uint8)]
+    _ip = ctypes.POINTER(ctypes.c_int)
+    L.oracle_table_row.argtypes = [ctypes.c_int] * 5 + [_c_double_p, ctypes.c_int, ctypes.c_int,
+                                                        _ip, _ip, _ip, _c_double_p]
     return L
 
 
@@ -250,3 +253,21 @@ def parity_error(got, expect, absmag, floor=1e-3):
     normwise = float(np.max(diff) / denom) if denom > 0 else float(np.max(diff))
     return (float(np.max(rel)), float(np.max(unfl)) if unfl.size else 0.0,
             normwise, float(np.mean(floored)))
+
+
+def table_row(T, s0, s1, r, n, abscissa, policy, step):
+    """(kind, node steps, weights) of `step` by simulating Algorithm 1:
+    kind 0 = full step, 1 = predicted from the listed entries."""
+    x = _f64(abscissa)
+    if x.size != T:
+        raise OracleError("one abscissa per step")
+    kind, n_used = ctypes.c_int(), ctypes.c_int()
+    nodes = (ctypes.c_int * 64)()
+    w = np.zeros(64, dtype=np.float64)
+    rc = lib().oracle_table_row(int(T), int(s0), int(s1), int(r), int(n),
+                                _ptr(x, ctypes.c_double), int(policy), int(step),
+                                ctypes.byref(kind), ctypes.byref(n_used), nodes,
+                                _ptr(w, ctypes.c_double))
+    if rc != 0:
+        raise OracleError(_NODE_ERRORS.get(rc, f"oracle error {rc}"))
+    return kind.value, [nodes[j] for j in range(n_used.value)], w[:n_used.value].copy()

@@ -283,3 +283,56 @@ int oracle_full_schedule(int T, int s0, int s1, int r, uint8_t *is_full) {
   }
   return count;
 }
+
+/* ------------------------------------------------------------------------ */
+/* Offline table by simulating the online stage (Algorithm 1).               */
+/* ------------------------------------------------------------------------ */
+
+/* What step `step` does under schedule (T, s0, s1, r) with history size n,
+ * found by running Algorithm 1's loop from step 0: a full step appends
+ * itself to the history H (dropping the oldest once H holds n entries); a
+ * skipped step with |H| = n gets the coefficients of the abscissae of H at
+ * its own abscissa.  A skipped step with |H| < n follows `policy`: 0 runs
+ * the full network instead (and so enters H), 1 uses the |H| entries it has
+ * (a lower-degree interpolant), or a full step if H is empty.
+ *   *kind     0 full, 1 predicted
+ *   *n_used   entries the prediction uses (0 for a full step)
+ *   nodes[]   their steps, oldest to newest;  w[] their coefficients.
+ * Returns 0, or a negative code (bad arguments, or oracle_weights_row's). */
+int oracle_table_row(int T, int s0, int s1, int r, int n, const double *abscissa,
+                     int policy, int step, int *kind, int *n_used, int *nodes,
+                     double *w) {
+  if (n < 1 || n > ORACLE_MAX_NODES || step < 0 || step >= T) return -1;
+  if (policy != 0 && policy != 1) return -1;
+  uint8_t full[4096];
+  if (T > 4096) return -1;
+  if (oracle_full_schedule(T, s0, s1, r, full) < 0) return -1;
+  int hist[ORACLE_MAX_NODES];
+  int count = 0;
+  for (int s = 0; s <= step; ++s) {
+    int runs_full = full[s] || count == 0 || (count < n && policy == 0);
+    if (s == step) {
+      if (runs_full) {
+        *kind = 0;
+        *n_used = 0;
+        return 0;
+      }
+      double x[ORACLE_MAX_NODES];
+      for (int j = 0; j < count; ++j) {
+        nodes[j] = hist[j];
+        x[j] = abscissa[hist[j]];
+      }
+      *kind = 1;
+      *n_used = count;
+      return oracle_weights_row(x, count, abscissa[s], w);
+    }
+    if (runs_full) {
+      if (count == n) {           /* drop the oldest */
+        for (int j = 1; j < n; ++j) hist[j - 1] = hist[j];
+        count -= 1;
+      }
+      hist[count++] = s;
+    }
+  }
+  return -1; /* not reached */
+}

@@ -42,6 +42,9 @@ void oracle_extrapolate_f64(const double *const *F, int n, const double *w,
                             int64_t count, double *out);
 
 int oracle_full_schedule(int T, int s0, int s1, int r, uint8_t *is_full);
+int oracle_table_row(int T, int s0, int s1, int r, int n, const double *abscissa,
+                     int policy, int step, int *kind, int *n_used, int *nodes,
+                     double *w);
 
 #ifdef __cplusplus
 }

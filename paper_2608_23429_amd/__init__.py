@@ -13,13 +13,16 @@ import numpy as np
 import torch
 
 from ._binding import (  # noqa: F401  (re-exported C entry points)
-    CHEB_BF16, CHEB_F32, CHEB_MAX_NODES, CHEB_MAX_OUTPUTS, CHEB_MAX_SLOTS, ChebError,
+    CHEB_BF16, CHEB_F32, CHEB_MAX_NODES, CHEB_MAX_OUTPUTS, CHEB_MAX_SLOTS, CHEB_SHORT_FULL,
+    CHEB_SHORT_LOWER, ChebError,
     cheb_cache_begin_push, cheb_cache_commit, cheb_cache_create, cheb_cache_destroy,
-    cheb_cache_entry, cheb_cache_history, cheb_cache_layout, cheb_cache_push,
+    cheb_cache_dtype, cheb_cache_entry, cheb_cache_history, cheb_cache_layout, cheb_cache_push,
     cheb_cache_reset, cheb_cache_segment_offset, cheb_cache_slot_numel, cheb_combine,
     cheb_combine_multi, cheb_extrapolate, cheb_extrapolate_at, cheb_extrapolate_at_multi,
-    cheb_extrapolate_multi, cheb_get_launch_config, cheb_last_error,
-    cheb_precompute_weights, cheb_set_launch_config, cheb_version,
+    cheb_extrapolate_multi, cheb_extrapolate_steps, cheb_get_launch_config, cheb_last_error,
+    cheb_precompute_weights, cheb_schedule, cheb_set_launch_config, cheb_table_build,
+    cheb_table_destroy, cheb_table_info, cheb_table_load, cheb_table_save, cheb_table_step,
+    cheb_version,
 )
 from . import _binding
 
@@ -83,6 +86,61 @@ def combine_multi(srcs: Sequence[torch.Tensor], w, outs: Sequence[torch.Tensor],
 
 def precompute_weights(hist_t, target_t) -> np.ndarray:
     return cheb_precompute_weights(hist_t, target_t)
+
+
+class ChebTable:
+    """The offline stage's weight table (schedule F, rows for every
+    predicted step), built in the library or loaded from a file."""
+
+    def __init__(self, T=None, s0=None, s1=None, r=None, n_hist=None, abscissa=None,
+                 policy=CHEB_SHORT_FULL, _handle=None):
+        if _handle is None:
+            _handle = cheb_table_build(T, s0, s1, r, n_hist, abscissa, policy)
+        self._h = _handle
+        info = cheb_table_info(self._h)
+        self.T, self.n_hist, self.policy, self.n_full = (
+            info["T"], info["n_hist"], info["policy"], info["n_full"])
+
+    @classmethod
+    def load(cls, path):
+        return cls(_handle=cheb_table_load(path))
+
+    def save(self, path):
+        cheb_table_save(self._h, path)
+
+    def step(self, s):
+        return cheb_table_step(self._h, s)
+
+    def runs(self):
+        """Consecutive predicted steps sharing one history: [(first, count)],
+        each cut to at most CHEB_MAX_OUTPUTS steps."""
+        out, s = [], 0
+        while s < self.T:
+            pred, nodes, _ = self.step(s)
+            if not pred:
+                s += 1
+                continue
+            first = s
+            while (s < self.T and s - first < CHEB_MAX_OUTPUTS and self.step(s)[0]
+                   and self.step(s)[1] == nodes):
+                s += 1
+            out.append((first, s - first))
+        return out
+
+    @property
+    def handle(self):
+        return self._h
+
+    def close(self):
+        if getattr(self, "_h", None) is not None:
+            cheb_table_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 class ChebCache:
@@ -205,6 +263,16 @@ class ChebCache:
                                       _stream_handle(stream), n_slots=self.n_slots)
         return outs, w
 
+    def extrapolate_steps(self, table: "ChebTable", first_step: int, n_steps: int = 1,
+                          outs: Optional[Sequence[torch.Tensor]] = None,
+                          stream: Optional[torch.cuda.Stream] = None):
+        outs = [self.new_output() for _ in range(n_steps)] if outs is None else list(outs)
+        for o in outs:
+            self._check_out(o)
+        cheb_extrapolate_steps(self._h, table.handle, first_step, [o.data_ptr() for o in outs],
+                               _stream_handle(stream))
+        return outs
+
     def extrapolate_at(self, target_t: float, out: Optional[torch.Tensor] = None,
                        stream: Optional[torch.cuda.Stream] = None):
         out = self.new_output() if out is None else out
@@ -215,5 +283,5 @@ class ChebCache:
 
 
 __all__ = [n for n in dir() if n.startswith("cheb_")] + [
-    "ChebCache", "ChebError", "combine", "combine_multi", "precompute_weights", "CHEB_BF16",
+    "ChebCache", "ChebTable", "ChebError", "combine", "combine_multi", "precompute_weights", "CHEB_BF16",
     "CHEB_F32", "CHEB_MAX_SLOTS", "CHEB_MAX_OUTPUTS", "CHEB_MAX_NODES", "LIB_PATH"]

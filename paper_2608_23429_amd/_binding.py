@@ -21,6 +21,10 @@ CHEB_E_ALIGN = -5
 CHEB_E_HIP = -6
 CHEB_E_MISMATCH = -7
 CHEB_E_NONFINITE = -8
+CHEB_E_IO = -9
+
+CHEB_SHORT_FULL = 0
+CHEB_SHORT_LOWER = 1
 
 CHEB_BF16 = 0
 CHEB_F32 = 1
@@ -33,6 +37,7 @@ STATUS_NAMES = {
     CHEB_E_NOTREADY: "CHEB_E_NOTREADY", CHEB_E_DTYPE: "CHEB_E_DTYPE",
     CHEB_E_ALIGN: "CHEB_E_ALIGN", CHEB_E_HIP: "CHEB_E_HIP",
     CHEB_E_MISMATCH: "CHEB_E_MISMATCH", CHEB_E_NONFINITE: "CHEB_E_NONFINITE",
+    CHEB_E_IO: "CHEB_E_IO",
 }
 
 
@@ -76,6 +81,15 @@ SIGNATURES = {
     "cheb_cache_entry": [_vp, ctypes.c_int32, _vpp],
     "cheb_cache_segment_offset": [_vp, ctypes.c_int32, _i64p],
     "cheb_cache_slot_numel": [_vp, _i64p],
+    "cheb_cache_dtype": [_vp, _i32p],
+    "cheb_schedule": [ctypes.c_int32] * 4 + [ctypes.POINTER(ctypes.c_uint8)],
+    "cheb_table_build": [ctypes.POINTER(_vp)] + [ctypes.c_int32] * 5 + [_dp, ctypes.c_int32],
+    "cheb_table_destroy": [_vp],
+    "cheb_table_info": [_vp, _i32p, _i32p, _i32p, _i32p],
+    "cheb_table_step": [_vp, ctypes.c_int32, _i32p, _i32p, _i32p, _dp],
+    "cheb_table_save": [_vp, ctypes.c_char_p],
+    "cheb_table_load": [ctypes.POINTER(_vp), ctypes.c_char_p],
+    "cheb_extrapolate_steps": [_vp, _vp, ctypes.c_int32, ctypes.c_int32, _vpp, _vp],
     "cheb_extrapolate": [_vp, _dp, _vp, _vp],
     "cheb_extrapolate_at": [_vp, ctypes.c_double, _vp, _vp, _dp],
     "cheb_extrapolate_multi": [_vp, _dp, ctypes.c_int32, _vpp, _vp],
@@ -221,6 +235,64 @@ def cheb_cache_slot_numel(handle) -> int:
     n = ctypes.c_int64()
     _check(LIB.cheb_cache_slot_numel(handle, ctypes.byref(n)))
     return n.value
+
+
+def cheb_cache_dtype(handle) -> int:
+    d = ctypes.c_int32()
+    _check(LIB.cheb_cache_dtype(handle, ctypes.byref(d)))
+    return d.value
+
+
+def cheb_schedule(T, s0, s1, r) -> np.ndarray:
+    """Boolean mask over steps 0..T-1 of the full-computation schedule."""
+    mask = np.zeros(int(T), dtype=np.uint8)
+    _check(LIB.cheb_schedule(int(T), int(s0), int(s1), int(r),
+                             mask.ctypes.data_as(ctypes.POINTER(ctypes.c_uint8))))
+    return mask.astype(bool)
+
+
+def cheb_table_build(T, s0, s1, r, n_hist, abscissa, policy=CHEB_SHORT_FULL):
+    x = _f64(abscissa).reshape(-1)
+    h = ctypes.c_void_p()
+    _check(LIB.cheb_table_build(ctypes.byref(h), int(T), int(s0), int(s1), int(r), int(n_hist),
+                                _dptr(x), int(policy)))
+    return h
+
+
+def cheb_table_destroy(table):
+    _check(LIB.cheb_table_destroy(table))
+
+
+def cheb_table_info(table):
+    T, n, p, f = (ctypes.c_int32() for _ in range(4))
+    _check(LIB.cheb_table_info(table, ctypes.byref(T), ctypes.byref(n), ctypes.byref(p),
+                               ctypes.byref(f)))
+    return {"T": T.value, "n_hist": n.value, "policy": p.value, "n_full": f.value}
+
+
+def cheb_table_step(table, step):
+    """(predicted, node steps, weights) of one step."""
+    pred, used = ctypes.c_int32(), ctypes.c_int32()
+    nodes = (ctypes.c_int32 * CHEB_MAX_SLOTS)()
+    w = np.zeros(CHEB_MAX_SLOTS, dtype=np.float64)
+    _check(LIB.cheb_table_step(table, int(step), ctypes.byref(pred), ctypes.byref(used), nodes,
+                               _dptr(w)))
+    return bool(pred.value), [nodes[j] for j in range(used.value)], w[:used.value].copy()
+
+
+def cheb_table_save(table, path):
+    _check(LIB.cheb_table_save(table, os.fsencode(path)))
+
+
+def cheb_table_load(path):
+    h = ctypes.c_void_p()
+    _check(LIB.cheb_table_load(ctypes.byref(h), os.fsencode(path)))
+    return h
+
+
+def cheb_extrapolate_steps(handle, table, first_step, out_ptrs, stream=0):
+    _check(LIB.cheb_extrapolate_steps(handle, table, int(first_step), len(out_ptrs),
+                                      _voidp_array(out_ptrs), ctypes.c_void_p(int(stream))))
 
 
 def cheb_extrapolate(handle, w, out_ptr, stream=0):

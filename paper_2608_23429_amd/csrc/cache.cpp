@@ -89,6 +89,34 @@ void record(cheb_cache *c, double t) {
 
 }  // namespace
 
+namespace cheb {
+
+// Prediction from the newest `used` held entries (oldest of them first).
+int extrapolate_newest(cheb_cache *c, int32_t used, const double *w, int32_t n_out,
+                       void *const *out, void *stream) {
+  if (!c || !w || !out) return fail(CHEB_E_INVAL, "cache, w or out is NULL");
+  if (c->push_open) return fail(CHEB_E_NOTREADY, "a fused push is open");
+  if (used < 1 || used > c->count)
+    return fail(CHEB_E_NOTREADY, "history holds %d entries, %d needed", c->count, used);
+  if (n_out < 1 || n_out > CHEB_MAX_OUTPUTS)
+    return fail(CHEB_E_INVAL, "n_out %d outside 1..%d", n_out, CHEB_MAX_OUTPUTS);
+  const void *src[CHEB_MAX_SLOTS];
+  for (int32_t j = 0; j < used; ++j) src[j] = c->slot_ptr(c->slot_of_age(c->count - used + j));
+  if (c->slot_numel > 0) {
+    const uintptr_t a0 = reinterpret_cast<uintptr_t>(c->arena);
+    const uintptr_t ob = uintptr_t(c->slot_numel) * uintptr_t(elem_bytes(c->dtype));
+    for (int32_t m = 0; m < n_out; ++m) {
+      if (!out[m]) return fail(CHEB_E_INVAL, "out[%d] is NULL", m);
+      const uintptr_t o0 = reinterpret_cast<uintptr_t>(out[m]);
+      if (o0 < a0 + c->arena_bytes && a0 < o0 + ob)
+        return fail(CHEB_E_INVAL, "out[%d] overlaps the cache arena", m);
+    }
+  }
+  return cheb_combine_multi(src, used, w, n_out, out, c->slot_numel, c->dtype, stream);
+}
+
+}  // namespace cheb
+
 extern "C" {
 
 int cheb_cache_layout(int32_t n_slots, int32_t dtype, const int64_t *seg_numel, int32_t n_segs,
@@ -217,6 +245,12 @@ int cheb_cache_segment_offset(const cheb_cache *c, int32_t seg, int64_t *elem_of
   return ok();
 }
 
+int cheb_cache_dtype(const cheb_cache *c, int32_t *dtype) {
+  if (!c || !dtype) return fail(CHEB_E_INVAL, "cache or dtype is NULL");
+  *dtype = c->dtype;
+  return ok();
+}
+
 int cheb_cache_slot_numel(const cheb_cache *c, int64_t *numel) {
   if (!c || !numel) return fail(CHEB_E_INVAL, "cache or numel is NULL");
   *numel = c->slot_numel;
@@ -225,25 +259,10 @@ int cheb_cache_slot_numel(const cheb_cache *c, int64_t *numel) {
 
 int cheb_extrapolate_multi(cheb_cache *c, const double *w, int32_t n_out, void *const *out,
                            void *stream) {
-  if (!c || !w || !out) return fail(CHEB_E_INVAL, "cache, w or out is NULL");
-  if (c->push_open) return fail(CHEB_E_NOTREADY, "a fused push is open");
-  if (c->count < c->n_slots)
+  if (!c) return fail(CHEB_E_INVAL, "cache is NULL");
+  if (!c->push_open && c->count < c->n_slots)
     return fail(CHEB_E_NOTREADY, "history holds %d of %d entries", c->count, c->n_slots);
-  if (n_out < 1 || n_out > CHEB_MAX_OUTPUTS)
-    return fail(CHEB_E_INVAL, "n_out %d outside 1..%d", n_out, CHEB_MAX_OUTPUTS);
-  const void *src[CHEB_MAX_SLOTS];
-  for (int32_t a = 0; a < c->n_slots; ++a) src[a] = c->slot_ptr(c->slot_of_age(a));
-  if (c->slot_numel > 0) {
-    const uintptr_t a0 = reinterpret_cast<uintptr_t>(c->arena);
-    const uintptr_t ob = uintptr_t(c->slot_numel) * uintptr_t(elem_bytes(c->dtype));
-    for (int32_t m = 0; m < n_out; ++m) {
-      if (!out[m]) return fail(CHEB_E_INVAL, "out[%d] is NULL", m);
-      const uintptr_t o0 = reinterpret_cast<uintptr_t>(out[m]);
-      if (o0 < a0 + c->arena_bytes && a0 < o0 + ob)
-        return fail(CHEB_E_INVAL, "out[%d] overlaps the cache arena", m);
-    }
-  }
-  return cheb_combine_multi(src, c->n_slots, w, n_out, out, c->slot_numel, c->dtype, stream);
+  return cheb::extrapolate_newest(c, c->n_slots, w, n_out, out, stream);
 }
 
 int cheb_extrapolate(cheb_cache *c, const double *w, void *out, void *stream) {

@@ -42,6 +42,11 @@ int weights_row(const double *x, int n, double target, double *w);
 int launch_combine(int dtype, const void *const *src, int n, const double *w, int n_out,
                    void *const *out, int64_t numel, hipStream_t stream);
 
+// Prediction from the newest `used` entries of the ring (oldest of them
+// first): out[m] = sum_j w[m * used + j] * entry_j, with the cache's checks.
+int extrapolate_newest(cheb_cache *c, int32_t used, const double *w, int32_t n_out,
+                       void *const *out, void *stream);
+
 // Segment copy into one slot; zero-fills each segment's padding up to the
 // next 16-byte boundary.
 struct GatherSeg {

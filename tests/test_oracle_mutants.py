@@ -44,6 +44,11 @@ MUTANTS = [
     ("rounding truncates", "if (frac > 0.5 ||", "if (frac > 1.5 ||", 0),
     ("schedule end off by one", "(s > T - 1 - s1)", "(s > T - s1)", 0),
     ("schedule grid offset", "((s - s0) % r) == 0", "((s - s0 + 1) % r) == 0", 0),
+    ("table keeps oldest", "for (int j = 1; j < n; ++j) hist[j - 1] = hist[j];",
+     "for (int j = 1; j < n - 1; ++j) hist[j] = hist[j + 1];", 0),
+    ("table ignores short-history policy", "(count < n && policy == 0)", "(count < n && policy == 1)", 0),
+    ("table uses step not abscissa", "return oracle_weights_row(x, count, abscissa[s], w);",
+     "return oracle_weights_row(x, count, abscissa[s] + 1.0, w);", 0),
 ]
 
 

@@ -348,3 +348,30 @@ def test_full_schedule_golden():
             assert int(mask.sum()) == int(tail), line
         n += 1
     assert n == 9
+
+
+def test_table_rows_golden():
+    """The oracle's Algorithm-1 simulation against hand-worked rows; the
+    coefficients of a predicted step are the (pinned) weights of its nodes."""
+    with open(os.path.join(GOLDEN, "table_rows.txt")) as f:
+        lines = [l.split("#")[0].strip() for l in f]
+    n_cases = 0
+    for line in lines:
+        if not line:
+            continue
+        head, tail = line.split(":")
+        T, s0, s1, r, n, policy = (int(v) for v in head.split())
+        items = tail.split()
+        assert len(items) == T
+        x = 999.0 - 37.0 * np.arange(T)             # any distinct abscissae
+        for s, item in enumerate(items):
+            kind, nodes, w = oracle.table_row(T, s0, s1, r, n, x, policy, s)
+            if item == "F":
+                assert kind == 0 and nodes == [], (line, s)
+            else:
+                want = [int(v) for v in item.split("+")]
+                assert kind == 1 and nodes == want, (line, s, nodes)
+                exact = lagrange_weights(x[want], x[s])
+                assert np.allclose(w, [float(e) for e in exact], rtol=0, atol=1e-12 * max(1, np.abs(w).sum()))
+        n_cases += 1
+    assert n_cases == 5
