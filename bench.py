@@ -165,6 +165,62 @@ def time_multi(torch, cfg, cache, steps, warmup):
                     "pass over the history (cheb_extrapolate_at_multi); not in value"}
 
 
+def time_residual(torch, cheb, cfg, entries, cache, steps, warmup):
+    """Skipped step's residual update x_out = x_in + (every predicted module
+    output added into the residual stream): the full form over the whole
+    history (cheb_residual_apply), and the collapsed history (push-time
+    reduction per full step, cheb_residual_reduce, then the prediction from
+    residual-sized entries)."""
+    from synth import split_segments
+    res_off, res_n = cfg.residual_map()
+    stream = torch.cuda.current_stream()
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    w = cheb.cheb_precompute_weights(cache.history(), [cfg.targets[0]])[0]
+    x_in = torch.randn(res_n, device="cuda")
+    x_out = torch.empty_like(x_in)
+
+    def timed(fn, n):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        a, b = ev(), ev()
+        a.record(stream)
+        for _ in range(n):
+            fn()
+        b.record(stream)
+        b.synchronize()
+        return a.elapsed_time(b) / n * 1e3
+
+    S = cfg.numel * cfg.elem_size
+    R = res_n * 4
+    us_full = timed(lambda: cache.residual_apply(w, res_off, x_out, x_in, stream=stream), steps)
+    hist = cheb.ResidualHistory(cfg.n_hist, res_off, res_n)
+    segs = [split_segments(e, cfg) for e in entries]
+    for x, sg in zip(cfg.nodes, segs):
+        hist.push(x, sg, stream=stream)
+    k = [0]
+
+    def push_one():
+        hist.push(cfg.nodes[k[0] % cfg.n_hist] + 1e-3 * (1 + k[0]), segs[k[0] % cfg.n_hist],
+                  stream=stream)
+        k[0] += 1
+    us_reduce = timed(push_one, max(5, steps // 5))
+    wc = cheb.cheb_precompute_weights(hist.history(), [float(hist.history()[-1]) - 0.02])[0]
+    us_pred = timed(lambda: hist.cache.residual_apply(wc, [0], x_out, x_in, stream=stream), steps)
+    hist.close()
+    return {
+        "full_form": {"us": us_full, "bytes": cfg.n_hist * S + 2 * R,
+                      "gbps": (cfg.n_hist * S + 2 * R) / (us_full * 1e3)},
+        "collapsed_push_reduce": {"us": us_reduce, "bytes": S + R, "gbps": (S + R) / (us_reduce * 1e3)},
+        "collapsed_predict": {"us": us_pred, "bytes": (cfg.n_hist + 2) * R,
+                              "gbps": (cfg.n_hist + 2) * R / (us_pred * 1e3)},
+        "residual_elements": res_n,
+        "note": "skipped-step residual update (block stack with every module output "
+                "predicted); full form reads the whole history, collapsed form keeps one "
+                "residual-sized fp32 entry per full step; not in value",
+    }
+
+
 def parity_sample(torch, cfg, entries, cache, out, target, count=1 << 16):
     import numpy as np
     import oracle
@@ -278,6 +334,10 @@ def main(argv=None):
     multi = time_multi(torch, cfg, cache, max(10, args.steps // 2), args.warmup)
     log(f"[bench] {cfg.name} multi-target: {multi['us_per_skipped_step']:.1f} us per skipped "
         f"step ({multi['gbps']:.0f} GB/s over {multi['targets_per_pass']} targets)")
+    resid = time_residual(torch, cheb, cfg, entries, cache, max(10, args.steps // 2), args.warmup)
+    log(f"[bench] {cfg.name} residual: full form {resid['full_form']['us']:.1f} us, collapsed "
+        f"predict {resid['collapsed_predict']['us']:.1f} us + push-time reduce "
+        f"{resid['collapsed_push_reduce']['us']:.1f} us per full step")
     par = parity_sample(torch, cfg, entries, cache, out, cfg.targets[-1])
     log(f"[bench] parity sample: floored error {par['floored_rel_err']:.3e}")
     achieved = res["bytes_per_step"] / (res["launch_us_avg"] * 1e3)
@@ -308,6 +368,7 @@ def main(argv=None):
         "push": {"us_median": res["push_us_median"], "gbps": res["push_gbps"],
                  "note": "full-step copy into the ring, once per full step (not in value)"},
         "multi_target": multi,
+        "residual": resid,
         "parity_sample": par,
     }
     if not args.no_cpu_baseline:

@@ -325,6 +325,52 @@ CHEB_API int cheb_extrapolate_steps(cheb_cache *c, const cheb_table *t, int32_t 
                                     int32_t n_steps, void *const *out, void *stream);
 
 /* ------------------------------------------------------------------------ */
+/* Residual application on a skipped step.                                   */
+/* ------------------------------------------------------------------------ */
+
+/* A DiT block adds its module outputs to the residual stream,
+ * x_{l+1} = x_l + S^l + C^l + M^l (Section 3.1, block equation).  On a skipped
+ * step every module output is the prediction sum_k w_k H_k[segment]
+ * (Section 3.3; Algorithm 1), so the whole block stack adds
+ *     x_out[j] = x_in[j] + sum over segments s with res_offset[s] >= 0 and
+ *                j in [res_offset[s], res_offset[s] + seg_numel[s]) of
+ *                sum_k w_k H_k[seg_offset[s] + j - res_offset[s]].
+ * This call forms it in one pass over the history: the per-module
+ * predictions are never written.  fp64 accumulation, fp32 residual.
+ *   w          [n_slots] host fp64, aligned with cheb_cache_history.
+ *   res_offset [n_segs] host: element of the residual where segment s adds;
+ *              negative: segment s is not added.  Offsets and segment sizes
+ *              of added segments are multiples of 16 bytes' worth of the
+ *              storage type (8 bf16 / 4 fp32 elements).
+ *   res_numel  elements of the residual (same multiple).
+ *   x_in       device fp32 [res_numel], 16-byte aligned, or NULL (zero);
+ *              it may be x_out itself (in place), not a partial overlap.
+ *   x_out      device fp32 [res_numel], 16-byte aligned, outside the arena.
+ * Requires a full history.  Errors: CHEB_E_INVAL, CHEB_E_NOTREADY,
+ * CHEB_E_ALIGN, CHEB_E_NONFINITE, CHEB_E_HIP. */
+CHEB_API int cheb_residual_apply(cheb_cache *c, const double *w, const int64_t *res_offset,
+                                 int64_t res_numel, const float *x_in, float *x_out,
+                                 void *stream);
+
+/* The same mapping applied to one full step's module outputs:
+ *     x_out[j] = x_in[j] + sum over added segments s covering j of
+ *                seg_src[s][j - res_offset[s]].
+ * Written into a slot of an fp32 cache with one segment of res_numel
+ * elements (cheb_cache_begin_push / cheb_cache_commit), it keeps a collapsed
+ * history: the block stack's total contribution per full step, from which
+ * cheb_residual_apply (res_offset = {0}) predicts a skipped step's residual
+ * at a cost of res_numel instead of the whole cache per entry.  Equal to
+ * the full form by linearity of the prediction.
+ *   seg_src [n_segs] device pointers, 16-byte aligned (NULL allowed for
+ *           segments not added), seg_numel[s] elements of `dtype` each.
+ * Other arguments as cheb_residual_apply.  Errors: CHEB_E_INVAL,
+ * CHEB_E_DTYPE, CHEB_E_ALIGN, CHEB_E_HIP. */
+CHEB_API int cheb_residual_reduce(const void *const *seg_src, const int64_t *seg_numel,
+                                  const int64_t *res_offset, int32_t n_segs, int32_t dtype,
+                                  const float *x_in, float *x_out, int64_t res_numel,
+                                  void *stream);
+
+/* ------------------------------------------------------------------------ */
 /* Launch shape (tuning).                                                    */
 /* ------------------------------------------------------------------------ */
 

@@ -77,6 +77,13 @@ def bind(path):
     L.oracle_extrapolate_f64.restype = None
     L.oracle_full_schedule.argtypes = [ctypes.c_int] * 4 + [
         ctypes.POINTER(ctypes.c_uint8)]
+    _i64 = ctypes.POINTER(ctypes.c_int64)
+    L.oracle_residual_bf16.argtypes = [ctypes.POINTER(_c_u16_p), ctypes.c_int, _c_double_p,
+                                       _i64, _i64, _i64, ctypes.c_int, _c_double_p,
+                                       ctypes.c_int64, _c_double_p, _c_double_p]
+    L.oracle_residual_f32.argtypes = [ctypes.POINTER(_c_f32_p), ctypes.c_int, _c_double_p,
+                                      _i64, _i64, _i64, ctypes.c_int, _c_double_p,
+                                      ctypes.c_int64, _c_double_p, _c_double_p]
     _ip = ctypes.POINTER(ctypes.c_int)
     L.oracle_table_row.argtypes = [ctypes.c_int] * 5 + [_c_double_p, ctypes.c_int, ctypes.c_int,
                                                         _ip, _ip, _ip, _c_double_p]
@@ -271,3 +278,35 @@ def table_row(T, s0, s1, r, n, abscissa, policy, step):
     if rc != 0:
         raise OracleError(_NODE_ERRORS.get(rc, f"oracle error {rc}"))
     return kind.value, [nodes[j] for j in range(n_used.value)], w[:n_used.value].copy()
+
+
+def residual(slots, w, slot_offset, seg_numel, res_offset, res_numel, x_in=None,
+             dtype="bf16"):
+    """x_in + sum over mapped segments of the predicted module outputs (fp64),
+    and the magnitude of its terms.  slots: history entries (uint16 patterns
+    for bf16, float32 for f32); res_offset[s] < 0 leaves segment s out."""
+    ctype = ctypes.c_uint16 if dtype == "bf16" else ctypes.c_float
+    np_t = np.uint16 if dtype == "bf16" else np.float32
+    arrs = [np.ascontiguousarray(a, dtype=np_t).reshape(-1) for a in slots]
+    w = _f64(w)
+    if len(w) != len(arrs):
+        raise OracleError("weight count differs from history size")
+    so = np.ascontiguousarray(slot_offset, dtype=np.int64)
+    sn = np.ascontiguousarray(seg_numel, dtype=np.int64)
+    ro = np.ascontiguousarray(res_offset, dtype=np.int64)
+    for a in arrs:
+        if np.any((so + sn > a.size) & (ro >= 0)):
+            raise OracleError("segment outside a history entry")
+    xi = None if x_in is None else _f64(x_in).reshape(-1)
+    out = np.empty(int(res_numel), dtype=np.float64)
+    mag = np.empty(int(res_numel), dtype=np.float64)
+    P = ctypes.POINTER(ctype)
+    ptrs = (P * len(arrs))(*[_ptr(a, ctype) for a in arrs])
+    fn = lib().oracle_residual_bf16 if dtype == "bf16" else lib().oracle_residual_f32
+    rc = fn(ptrs, len(arrs), _ptr(w, ctypes.c_double), _ptr(so, ctypes.c_int64),
+            _ptr(sn, ctypes.c_int64), _ptr(ro, ctypes.c_int64), len(sn),
+            None if xi is None else _ptr(xi, ctypes.c_double), int(res_numel),
+            _ptr(out, ctypes.c_double), _ptr(mag, ctypes.c_double))
+    if rc != 0:
+        raise OracleError("segment outside the residual")
+    return out, mag

@@ -336,3 +336,74 @@ int oracle_table_row(int T, int s0, int s1, int r, int n, const double *abscissa
   }
   return -1; /* not reached */
 }
+
+/* ------------------------------------------------------------------------ */
+/* Residual application on a skipped step (Section 3.1, block equation).     */
+/* ------------------------------------------------------------------------ */
+
+/* A DiT block adds its module outputs to the residual stream:
+ * x_{l+1} = x_l + S^l + C^l + M^l.  On a skipped step every module output
+ * is the prediction sum_k w_k F_k[segment], so after all blocks
+ *     x_out[j] = x_in[j] + sum over segments s covering j of
+ *                sum_k w_k F_k[slot_offset[s] + (j - res_offset[s])].
+ * F_k are n history entries of slot_numel elements (bfloat16 bit patterns),
+ * segment s holds seg_numel[s] elements at slot_offset[s] and adds into
+ * residual elements res_offset[s] .. res_offset[s] + seg_numel[s] - 1
+ * (res_offset[s] < 0: the segment is not added).  x_in may be NULL (zero).
+ * absmag (may be NULL) receives |x_in[j]| + the sum of |w_k| |F_k[.]| over
+ * the same terms.  Everything in fp64, segment by segment, oldest entry
+ * first.  Returns 0, or -1 if a segment leaves the residual. */
+int oracle_residual_bf16(const uint16_t *const *F, int n, const double *w,
+                         const int64_t *slot_offset, const int64_t *seg_numel,
+                         const int64_t *res_offset, int n_segs, const double *x_in,
+                         int64_t res_numel, double *x_out, double *absmag) {
+  for (int s = 0; s < n_segs; ++s)
+    if (res_offset[s] >= 0 && res_offset[s] + seg_numel[s] > res_numel) return -1;
+  for (int64_t j = 0; j < res_numel; ++j) {
+    x_out[j] = x_in ? x_in[j] : 0.0;
+    if (absmag) absmag[j] = x_in ? fabs(x_in[j]) : 0.0;
+  }
+  for (int s = 0; s < n_segs; ++s) {
+    if (res_offset[s] < 0) continue;
+#pragma omp parallel for schedule(static)
+    for (int64_t e = 0; e < seg_numel[s]; ++e) {
+      double acc = 0.0, mag = 0.0;
+      for (int k = 0; k < n; ++k) {
+        double f = oracle_bf16_to_f64(F[k][slot_offset[s] + e]);
+        acc += w[k] * f;
+        mag += fabs(w[k]) * fabs(f);
+      }
+      x_out[res_offset[s] + e] += acc;
+      if (absmag) absmag[res_offset[s] + e] += mag;
+    }
+  }
+  return 0;
+}
+
+/* The same with binary32 history entries. */
+int oracle_residual_f32(const float *const *F, int n, const double *w,
+                        const int64_t *slot_offset, const int64_t *seg_numel,
+                        const int64_t *res_offset, int n_segs, const double *x_in,
+                        int64_t res_numel, double *x_out, double *absmag) {
+  for (int s = 0; s < n_segs; ++s)
+    if (res_offset[s] >= 0 && res_offset[s] + seg_numel[s] > res_numel) return -1;
+  for (int64_t j = 0; j < res_numel; ++j) {
+    x_out[j] = x_in ? x_in[j] : 0.0;
+    if (absmag) absmag[j] = x_in ? fabs(x_in[j]) : 0.0;
+  }
+  for (int s = 0; s < n_segs; ++s) {
+    if (res_offset[s] < 0) continue;
+#pragma omp parallel for schedule(static)
+    for (int64_t e = 0; e < seg_numel[s]; ++e) {
+      double acc = 0.0, mag = 0.0;
+      for (int k = 0; k < n; ++k) {
+        double f = (double)F[k][slot_offset[s] + e];
+        acc += w[k] * f;
+        mag += fabs(w[k]) * fabs(f);
+      }
+      x_out[res_offset[s] + e] += acc;
+      if (absmag) absmag[res_offset[s] + e] += mag;
+    }
+  }
+  return 0;
+}

@@ -46,6 +46,15 @@ int oracle_table_row(int T, int s0, int s1, int r, int n, const double *abscissa
                      int policy, int step, int *kind, int *n_used, int *nodes,
                      double *w);
 
+int oracle_residual_bf16(const uint16_t *const *F, int n, const double *w,
+                         const int64_t *slot_offset, const int64_t *seg_numel,
+                         const int64_t *res_offset, int n_segs, const double *x_in,
+                         int64_t res_numel, double *x_out, double *absmag);
+int oracle_residual_f32(const float *const *F, int n, const double *w,
+                        const int64_t *slot_offset, const int64_t *seg_numel,
+                        const int64_t *res_offset, int n_segs, const double *x_in,
+                        int64_t res_numel, double *x_out, double *absmag);
+
 #ifdef __cplusplus
 }
 #endif

@@ -20,7 +20,8 @@ from ._binding import (  # noqa: F401  (re-exported C entry points)
     cheb_cache_reset, cheb_cache_segment_offset, cheb_cache_slot_numel, cheb_combine,
     cheb_combine_multi, cheb_extrapolate, cheb_extrapolate_at, cheb_extrapolate_at_multi,
     cheb_extrapolate_multi, cheb_extrapolate_steps, cheb_get_launch_config, cheb_last_error,
-    cheb_precompute_weights, cheb_schedule, cheb_set_launch_config, cheb_table_build,
+    cheb_precompute_weights, cheb_residual_apply, cheb_residual_reduce, cheb_schedule,
+    cheb_set_launch_config, cheb_table_build,
     cheb_table_destroy, cheb_table_info, cheb_table_load, cheb_table_save, cheb_table_step,
     cheb_version,
 )
@@ -141,6 +142,56 @@ class ChebTable:
             self.close()
         except Exception:
             pass
+
+
+def residual_reduce(segments: Sequence[torch.Tensor], res_offset, x_out: torch.Tensor,
+                    x_in: Optional[torch.Tensor] = None,
+                    stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+    """x_out = x_in + the mapped sum of one step's module outputs."""
+    dt = cheb_dtype(segments[0].dtype)
+    for i, t in enumerate(segments):
+        _check_device_tensor(t, f"segments[{i}]")
+        if t.dtype != segments[0].dtype:
+            raise ChebError(_binding.CHEB_E_MISMATCH, "segments differ in dtype")
+    _check_device_tensor(x_out, "x_out")
+    cheb_residual_reduce([t.data_ptr() for t in segments], [t.numel() for t in segments],
+                         res_offset, dt, None if x_in is None else x_in.data_ptr(),
+                         x_out.data_ptr(), x_out.numel(), _stream_handle(stream))
+    return x_out
+
+
+class ResidualHistory:
+    """Collapsed history: per full step, only the block stack's total
+    contribution to the residual stream (fp32), in a ring of n entries.  A
+    skipped step's residual is x_in plus the prediction from these entries,
+    which by linearity equals the sum of every module's prediction."""
+
+    def __init__(self, n_slots: int, res_offset: Sequence[int], res_numel: int, device=None):
+        self.res_offset = [int(o) for o in res_offset]
+        self.res_numel = int(res_numel)
+        self.cache = ChebCache(n_slots, torch.float32, [self.res_numel], device=device)
+
+    def push(self, t: float, segments: Sequence[torch.Tensor],
+             stream: Optional[torch.cuda.Stream] = None):
+        slot = self.cache.begin_push()
+        try:
+            residual_reduce(segments, self.res_offset, slot[:self.res_numel], stream=stream)
+        except Exception:
+            self.cache.reset()
+            raise
+        self.cache.commit(t)
+
+    def history(self):
+        return self.cache.history()
+
+    def predict(self, target_t: float, x_out: torch.Tensor, x_in: Optional[torch.Tensor] = None,
+                stream: Optional[torch.cuda.Stream] = None):
+        w = cheb_precompute_weights(self.history(), [target_t])[0]
+        self.cache.residual_apply(w, [0], x_out, x_in, stream=stream)
+        return x_out, w
+
+    def close(self):
+        self.cache.close()
 
 
 class ChebCache:
@@ -273,6 +324,22 @@ class ChebCache:
                                _stream_handle(stream))
         return outs
 
+    def residual_apply(self, w, res_offset, x_out: torch.Tensor,
+                       x_in: Optional[torch.Tensor] = None,
+                       stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+        """x_out = x_in + the block stack's predicted module outputs (one pass)."""
+        _check_device_tensor(x_out, "x_out")
+        if x_out.dtype != torch.float32:
+            raise ChebError(_binding.CHEB_E_DTYPE, "the residual is float32")
+        if x_in is not None:
+            _check_device_tensor(x_in, "x_in")
+            if x_in.dtype != torch.float32 or x_in.numel() != x_out.numel():
+                raise ChebError(_binding.CHEB_E_MISMATCH, "x_in differs from x_out")
+        cheb_residual_apply(self._h, w, res_offset, x_out.numel(),
+                            None if x_in is None else x_in.data_ptr(), x_out.data_ptr(),
+                            _stream_handle(stream))
+        return x_out
+
     def extrapolate_at(self, target_t: float, out: Optional[torch.Tensor] = None,
                        stream: Optional[torch.cuda.Stream] = None):
         out = self.new_output() if out is None else out
@@ -283,5 +350,5 @@ class ChebCache:
 
 
 __all__ = [n for n in dir() if n.startswith("cheb_")] + [
-    "ChebCache", "ChebTable", "ChebError", "combine", "combine_multi", "precompute_weights", "CHEB_BF16",
+    "ChebCache", "ChebTable", "ChebError", "ResidualHistory", "residual_reduce", "combine", "combine_multi", "precompute_weights", "CHEB_BF16",
     "CHEB_F32", "CHEB_MAX_SLOTS", "CHEB_MAX_OUTPUTS", "CHEB_MAX_NODES", "LIB_PATH"]

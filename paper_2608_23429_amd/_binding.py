@@ -94,6 +94,9 @@ SIGNATURES = {
     "cheb_extrapolate_at": [_vp, ctypes.c_double, _vp, _vp, _dp],
     "cheb_extrapolate_multi": [_vp, _dp, ctypes.c_int32, _vpp, _vp],
     "cheb_extrapolate_at_multi": [_vp, _dp, ctypes.c_int32, _vpp, _vp, _dp],
+    "cheb_residual_apply": [_vp, _dp, _i64p, ctypes.c_int64, _vp, _vp, _vp],
+    "cheb_residual_reduce": [_vpp, _i64p, _i64p, ctypes.c_int32, ctypes.c_int32, _vp, _vp,
+                             ctypes.c_int64, _vp],
     "cheb_get_launch_config": [ctypes.POINTER(cheb_launch_config)],
     "cheb_set_launch_config": [ctypes.POINTER(cheb_launch_config)],
 }
@@ -323,6 +326,25 @@ def cheb_extrapolate_at_multi(handle, targets, out_ptrs, stream=0, n_slots=CHEB_
     _check(LIB.cheb_extrapolate_at_multi(handle, _dptr(t), t.size, _voidp_array(out_ptrs),
                                          ctypes.c_void_p(int(stream)), _dptr(w)))
     return w.reshape(-1)[:t.size * n_slots].reshape(t.size, n_slots).copy()
+
+
+def cheb_residual_apply(handle, w, res_offset, res_numel, x_in_ptr, x_out_ptr, stream=0):
+    w = _f64(w).reshape(-1)
+    ro = np.ascontiguousarray(res_offset, dtype=np.int64).reshape(-1)
+    _check(LIB.cheb_residual_apply(handle, _dptr(w), ro.ctypes.data_as(_i64p), int(res_numel),
+                                   ctypes.c_void_p(int(x_in_ptr or 0)),
+                                   ctypes.c_void_p(int(x_out_ptr)), ctypes.c_void_p(int(stream))))
+
+
+def cheb_residual_reduce(seg_ptrs, seg_numel, res_offset, dtype, x_in_ptr, x_out_ptr, res_numel,
+                         stream=0):
+    sn = np.ascontiguousarray(seg_numel, dtype=np.int64).reshape(-1)
+    ro = np.ascontiguousarray(res_offset, dtype=np.int64).reshape(-1)
+    _check(LIB.cheb_residual_reduce(_voidp_array(seg_ptrs), sn.ctypes.data_as(_i64p),
+                                    ro.ctypes.data_as(_i64p), sn.size, int(dtype),
+                                    ctypes.c_void_p(int(x_in_ptr or 0)),
+                                    ctypes.c_void_p(int(x_out_ptr)), int(res_numel),
+                                    ctypes.c_void_p(int(stream))))
 
 
 def cheb_get_launch_config():

@@ -20,7 +20,7 @@ BUILD_DIR = os.path.join(ROOT, "_build", "cheb")
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 ARCH = "gfx950"
 
-HOST_SOURCES = ["api.cpp", "cache.cpp", "table.cpp"]
+HOST_SOURCES = ["api.cpp", "cache.cpp", "table.cpp", "residual.cpp"]
 DEVICE_SOURCES = ["kernels.hip"]
 
 DEVICE_FLAGS = [

@@ -115,6 +115,21 @@ int extrapolate_newest(cheb_cache *c, int32_t used, const double *w, int32_t n_o
   return cheb_combine_multi(src, used, w, n_out, out, c->slot_numel, c->dtype, stream);
 }
 
+int cache_view(const cheb_cache *c, CacheView *v) {
+  if (!c || !v) return fail(CHEB_E_INVAL, "cache is NULL");
+  v->n_slots = c->n_slots;
+  v->dtype = c->dtype;
+  v->count = c->count;
+  v->n_segs = int32_t(c->seg_numel.size());
+  v->push_open = c->push_open;
+  v->seg_numel = c->seg_numel.data();
+  v->seg_offset = c->seg_offset.data();
+  v->slot_numel = c->slot_numel;
+  v->arena = c->arena;
+  v->arena_bytes = c->arena_bytes;
+  return CHEB_OK;
+}
+
 }  // namespace cheb
 
 extern "C" {

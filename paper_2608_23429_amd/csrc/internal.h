@@ -57,4 +57,24 @@ struct GatherSeg {
 int launch_gather(int dtype, void *slot_base, const GatherSeg *segs, int n_segs,
                   hipStream_t stream);
 
+// Read-only view of a cache's layout and ring state (cache.cpp).
+struct CacheView {
+  int32_t n_slots, dtype, count, n_segs;
+  bool push_open;
+  const int64_t *seg_numel, *seg_offset;
+  int64_t slot_numel;
+  const char *arena;
+  size_t arena_bytes;
+};
+int cache_view(const cheb_cache *c, CacheView *v);
+
+// Residual kernel (kernels.hip): x_out[j] = x_in[j] + sum over the ncover
+// byte offsets delta[c] and entries k < n of w[k] * src(base[k] + delta[c] +
+// 16 * j), for residual vectors j in [vec_begin, vec_begin + n_vec).
+// ncover <= residual_max_cover(); vector indices below 2^31.
+int residual_max_cover();
+int launch_residual(int dtype, int n, const uint64_t *base, const double *w,
+                    const int64_t *delta, int ncover, const float *x_in, float *x_out,
+                    int64_t vec_begin, int64_t n_vec, hipStream_t stream);
+
 }  // namespace cheb

@@ -14,6 +14,9 @@
 //    (v_cvt_pk_bf16_f32).  No LDS: nothing is reused across lanes.
 // 2. The full-step push (Algorithm 1, full computation: store (s, f_s) in
 //    the history): one launch copies up to 64 segments into a slot.
+// 3. Residual application on a skipped step (Section 3.1, block equation):
+//    the block stack's sum of predicted module outputs added to the
+//    residual stream in one pass.
 #include <hip/hip_runtime.h>
 
 #include <stdint.h>
@@ -335,6 +338,145 @@ __global__ __launch_bounds__(kBlock) void gather_kernel(GatherArgs a, char *__re
   }
 }
 
+// ---- residual application on a skipped step ---------------------------------
+//
+// A DiT block adds its module outputs to the residual stream (Section 3.1,
+// block equation).  When every module output of a step is predicted, the
+// block stack adds sum_k w_k H_k[segment] for every cached segment, so
+//     x_out[j] = x_in[j] + sum_{segments s covering j} sum_k w_k H_k[s, j]
+// can be formed in one pass that reads the history once and never writes
+// the per-module predictions.  One launch covers one interval of the
+// residual on which the set of covering segments is constant (all of it for
+// DiT; the text and image parts for FLUX).  The covering segments travel as
+// byte offsets in the kernel arguments: entry k's element j of segment s is
+// at base[k] + delta[s] + 16 * (vector index of j).  Accumulation is fp64
+// (hundreds of terms per element), output fp32.
+
+struct Bf16Dec {
+  static constexpr int kVec = 8;
+  __device__ __forceinline__ static void add(double (&a)[8], u32x4 v, double w) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      a[2 * q] = fma(w, double(__uint_as_float(v[q] << 16)), a[2 * q]);
+      a[2 * q + 1] = fma(w, double(__uint_as_float(v[q] & 0xffff0000u)), a[2 * q + 1]);
+    }
+  }
+};
+
+struct F32Dec {
+  static constexpr int kVec = 4;
+  __device__ __forceinline__ static void add(double (&a)[4], u32x4 v, double w) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) a[q] = fma(w, double(__uint_as_float(v[q])), a[q]);
+  }
+};
+
+constexpr int kResCover = 128;
+constexpr int kResBlock = 256;
+
+template <int NS>
+struct ResArgs {
+  uint64_t base[NS];
+  double w[NS];
+  int64_t delta[kResCover];
+  const float *x_in;  // may be null: zero
+  float *x_out;
+  uint32_t vec_begin;
+  uint32_t n_vec;
+  int32_t ncover;
+};
+
+template <class Dec, int NS>
+__global__ __launch_bounds__(kResBlock) void residual_kernel(ResArgs<NS> a) {
+  constexpr int V = Dec::kVec;
+  const uint32_t i = blockIdx.x * uint32_t(kResBlock) + threadIdx.x;
+  if (i >= a.n_vec) return;
+  const uint64_t j = uint64_t(a.vec_begin) + i;  // residual vector index
+  double acc[V];
+  if (a.x_in) {
+    const u32x4 *xi = reinterpret_cast<const u32x4 *>(a.x_in + j * V);
+#pragma unroll
+    for (int h = 0; h < V / 4; ++h) {
+      const u32x4 x = xi[h];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) acc[4 * h + q] = double(__uint_as_float(x[q]));
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < V; ++e) acc[e] = 0.0;
+  }
+  const uint64_t off = j * 16u;
+  int32_t s = 0;
+  for (; s + 1 < a.ncover; s += 2) {  // two segments' loads in flight
+    u32x4 v0[NS], v1[NS];
+#pragma unroll
+    for (int k = 0; k < NS; ++k) {
+      v0[k] = __builtin_nontemporal_load(
+          reinterpret_cast<const u32x4 *>(a.base[k] + uint64_t(a.delta[s]) + off));
+      v1[k] = __builtin_nontemporal_load(
+          reinterpret_cast<const u32x4 *>(a.base[k] + uint64_t(a.delta[s + 1]) + off));
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int k = 0; k < NS; ++k) {
+      Dec::add(acc, v0[k], a.w[k]);
+      Dec::add(acc, v1[k], a.w[k]);
+    }
+  }
+  if (s < a.ncover) {
+    u32x4 v0[NS];
+#pragma unroll
+    for (int k = 0; k < NS; ++k)
+      v0[k] = __builtin_nontemporal_load(
+          reinterpret_cast<const u32x4 *>(a.base[k] + uint64_t(a.delta[s]) + off));
+#pragma unroll
+    for (int k = 0; k < NS; ++k) Dec::add(acc, v0[k], a.w[k]);
+  }
+  u32x4 *xo = reinterpret_cast<u32x4 *>(a.x_out + j * V);
+#pragma unroll
+  for (int h = 0; h < V / 4; ++h) {
+    u32x4 r;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) r[q] = __float_as_uint(float(acc[4 * h + q]));
+    xo[h] = r;
+  }
+}
+
+template <class Dec, int NS>
+hipError_t launch_residual_ns(const uint64_t *base, const double *w, const int64_t *delta,
+                              int ncover, const float *x_in, float *x_out, uint32_t vec_begin,
+                              uint32_t n_vec, hipStream_t s) {
+  ResArgs<NS> a;
+  memset(&a, 0, sizeof a);
+  for (int k = 0; k < NS; ++k) {
+    a.base[k] = base[k];
+    a.w[k] = w[k];
+  }
+  for (int c = 0; c < ncover; ++c) a.delta[c] = delta[c];
+  a.x_in = x_in;
+  a.x_out = x_out;
+  a.vec_begin = vec_begin;
+  a.n_vec = n_vec;
+  a.ncover = ncover;
+  const uint32_t grid = (n_vec + kResBlock - 1) / kResBlock;
+  hipLaunchKernelGGL((residual_kernel<Dec, NS>), dim3(grid), dim3(kResBlock), 0, s, a);
+  return hipGetLastError();
+}
+
+template <class Dec>
+hipError_t launch_residual_dec(int n, const uint64_t *base, const double *w, const int64_t *delta,
+                               int ncover, const float *x_in, float *x_out, uint32_t vec_begin,
+                               uint32_t n_vec, hipStream_t s) {
+  switch (n) {
+#define CHEB_RES_CASE(N) \
+  case N: return launch_residual_ns<Dec, N>(base, w, delta, ncover, x_in, x_out, vec_begin, n_vec, s);
+    CHEB_RES_CASE(1) CHEB_RES_CASE(2) CHEB_RES_CASE(3) CHEB_RES_CASE(4)
+    CHEB_RES_CASE(5) CHEB_RES_CASE(6) CHEB_RES_CASE(7)
+#undef CHEB_RES_CASE
+    default: return launch_residual_ns<Dec, 8>(base, w, delta, ncover, x_in, x_out, vec_begin, n_vec, s);
+  }
+}
+
 }  // namespace
 
 int launch_combine(int dtype, const void *const *src, int n, const double *w, int n_out,
@@ -383,6 +525,25 @@ int launch_gather(int dtype, void *slot_base, const GatherSeg *segs, int n_segs,
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return fail(CHEB_E_HIP, "push launch failed: %s", hipGetErrorString(e));
   }
+  return ok();
+}
+
+}  // namespace cheb
+
+namespace cheb {
+
+int residual_max_cover() { return kResCover; }
+
+int launch_residual(int dtype, int n, const uint64_t *base, const double *w, const int64_t *delta,
+                    int ncover, const float *x_in, float *x_out, int64_t vec_begin,
+                    int64_t n_vec, hipStream_t stream) {
+  if (n_vec == 0) return ok();
+  hipError_t e = dtype == CHEB_BF16
+                     ? launch_residual_dec<Bf16Dec>(n, base, w, delta, ncover, x_in, x_out,
+                                                    uint32_t(vec_begin), uint32_t(n_vec), stream)
+                     : launch_residual_dec<F32Dec>(n, base, w, delta, ncover, x_in, x_out,
+                                                   uint32_t(vec_begin), uint32_t(n_vec), stream);
+  if (e != hipSuccess) return fail(CHEB_E_HIP, "residual launch failed: %s", hipGetErrorString(e));
   return ok();
 }
 

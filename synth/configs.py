@@ -69,6 +69,41 @@ class Config:
             names = tuple(f"seg{i}" for i in range(len(segments)))
         return replace(self, segments=segments, segment_names=tuple(names))
 
+    def residual_map(self):
+        """Where each cached output adds into the residual stream, as
+        (res_offset per segment, residual elements).  DiT and PixArt blocks
+        add both outputs into the one token stream; FLUX double-stream
+        blocks add text outputs into the text tokens (first) and image
+        outputs into the image tokens (after them), single-stream blocks
+        into the joint stream."""
+        names = self.segment_names
+        if any(n.startswith("double") for n in names):
+            txt = [n for n, name in zip(self.seg_numel, names) if name.endswith(".txt")]
+            img = [n for n, name in zip(self.seg_numel, names) if name.endswith(".img")]
+            single = [n for n, name in zip(self.seg_numel, names) if name.startswith("single")]
+            n_txt, n_img = txt[0], img[0]
+            n_res = single[0] if single else n_txt + n_img
+            assert n_txt + n_img == n_res, "joint stream is text + image tokens"
+            offs = [n_txt if name.endswith(".img") else 0 for name in names]
+            return offs, n_res
+        n_res = self.seg_numel[0]
+        assert all(n == n_res for n in self.seg_numel), "one residual stream"
+        return [0] * len(names), n_res
+
+    def scaled_blocks(self, token_div: int, max_blocks: int) -> "Config":
+        """Same model structure with fewer blocks and fewer tokens (leading
+        dimensions divided by token_div), so residual maps stay consistent."""
+        segs, names = [], []
+        for shape, name in zip(self.segments, self.segment_names):
+            block = int("".join(ch for ch in name.split(".")[0] if ch.isdigit()) or 0)
+            if block >= max_blocks:
+                continue
+            new = list(shape)
+            new[-2] = max(1, new[-2] // token_div)
+            segs.append(tuple(new))
+            names.append(name)
+        return self.with_segments(segs, names)
+
     def shrunk(self, max_numel: int) -> "Config":
         """Same history, schedule and generator on a smaller cache.
 

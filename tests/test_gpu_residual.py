@@ -1,0 +1,189 @@
+"""Residual application on a skipped step (block equation of Section 3.1
+with every module output predicted) and the collapsed history, through the
+C ABI, against the oracle's plain per-segment fp64 definition."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_23429_amd as cheb
+from synth import CONFIGS, make_history, split_segments
+from tests.gpu_util import say, to_host_bits
+
+pytestmark = pytest.mark.gpu
+
+DT = {"bf16": torch.bfloat16, "f32": torch.float32}
+RES_TOL = 1e-5      # fp64 accumulation, one fp32 rounding of the result
+COLLAPSED_TOL = 1e-2  # bfloat16-storage bound; entries rounded once to fp32
+
+
+def _check(got, expect, mag, tol, label):
+    e = oracle.parity_error(np.asarray(got, dtype=np.float64), expect, mag)[0]
+    say(f"  {label}: floored error {e:.3e}")
+    assert e <= tol, (label, e)
+    return e
+
+
+def _fill(cfg, nodes, seed_shift=0):
+    entries = make_history(cfg, "cuda", nodes=nodes, seed=cfg.seed + seed_shift)
+    cache = cheb.ChebCache(len(nodes), DT[cfg.dtype], cfg.seg_numel)
+    for x, e in zip(nodes, entries):
+        cache.push(x, split_segments(e, cfg))
+    return entries, cache
+
+
+def _x_in(n, seed):
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    return torch.randn(n, generator=g, device="cuda") * 3.0
+
+
+SMALL = [
+    ("dit", lambda: CONFIGS[1].scaled_blocks(16, 4)),
+    ("pixart", lambda: CONFIGS[3].scaled_blocks(64, 3)),
+    ("flux", lambda: CONFIGS[4].scaled_blocks(32, 3)),
+    ("tiny", lambda: CONFIGS[0]),
+]
+
+
+@pytest.mark.parametrize("case", SMALL, ids=lambda c: c[0])
+def test_residual_apply_small(case):
+    cfg = case[1]()
+    res_off, res_n = cfg.residual_map()
+    entries, cache = _fill(cfg, cfg.nodes)
+    hosts = [to_host_bits(e) for e in entries]
+    t = cfg.targets[-1]
+    w = cheb.cheb_precompute_weights(cache.history(), [t])[0]
+    x_in = _x_in(res_n, 7)
+    x_out = torch.empty_like(x_in)
+    say(f"residual {case[0]}: {len(cfg.segments)} segments, residual {res_n}")
+    cache.residual_apply(w, res_off, x_out, x_in)
+    torch.cuda.synchronize()
+    w_or = oracle.weights_row(cfg.nodes, t)
+    exp, mag = oracle.residual(hosts, w_or, cache.seg_offset, cache.seg_numel, res_off, res_n,
+                               x_in=x_in.cpu().numpy(), dtype=cfg.dtype)
+    _check(x_out.cpu().numpy(), exp, mag, RES_TOL, "with x_in")
+    # no x_in, and in place
+    cache.residual_apply(w, res_off, x_out, None)
+    torch.cuda.synchronize()
+    exp0, mag0 = oracle.residual(hosts, w_or, cache.seg_offset, cache.seg_numel, res_off, res_n,
+                                 dtype=cfg.dtype)
+    _check(x_out.cpu().numpy(), exp0, mag0, RES_TOL, "x_in = NULL")
+    y = x_in.clone()
+    cache.residual_apply(w, res_off, y, y)
+    torch.cuda.synchronize()
+    _check(y.cpu().numpy(), exp, mag, RES_TOL, "in place")
+    cache.close()
+
+
+def test_residual_more_segments_than_one_launch_holds():
+    """300 segments over one residual: the covering list is split across
+    launches that accumulate in place."""
+    L = 4096
+    cfg = CONFIGS[1].with_segments([(1, 4, 1024)] * 300)
+    entries, cache = _fill(cfg, cfg.nodes)
+    w = cheb.cheb_precompute_weights(cache.history(), [cfg.targets[0]])[0]
+    x_out = torch.empty(L, dtype=torch.float32, device="cuda")
+    cache.residual_apply(w, [0] * 300, x_out, None)
+    torch.cuda.synchronize()
+    exp, mag = oracle.residual([to_host_bits(e) for e in entries],
+                               oracle.weights_row(cfg.nodes, cfg.targets[0]),
+                               cache.seg_offset, cache.seg_numel, [0] * 300, L)
+    _check(x_out.cpu().numpy(), exp, mag, RES_TOL, "300 segments")
+    cache.close()
+
+
+def test_residual_partial_coverage_and_unmapped_segments():
+    """Segments covering different parts of the residual, one left out."""
+    cfg = CONFIGS[3].with_segments([(64, 8), (32, 8), (16, 8), (64, 8), (8, 8)])
+    res_off = [0, 256, 128, 0, -1]
+    L = 64 * 8
+    entries, cache = _fill(cfg, cfg.nodes)
+    w = cheb.cheb_precompute_weights(cache.history(), [cfg.targets[1]])[0]
+    x_in = _x_in(L, 3)
+    x_out = torch.empty_like(x_in)
+    cache.residual_apply(w, res_off, x_out, x_in)
+    torch.cuda.synchronize()
+    exp, mag = oracle.residual([to_host_bits(e) for e in entries],
+                               oracle.weights_row(cfg.nodes, cfg.targets[1]),
+                               cache.seg_offset, cache.seg_numel, res_off, L,
+                               x_in=x_in.cpu().numpy())
+    _check(x_out.cpu().numpy(), exp, mag, RES_TOL, "partial coverage")
+    cache.close()
+
+
+@pytest.mark.parametrize("case", SMALL[:3], ids=lambda c: c[0])
+def test_collapsed_history_equals_full_form(case):
+    """Push-time reduction into a residual-sized fp32 ring, then the skipped
+    step's residual from it, against the oracle on the full history."""
+    cfg = case[1]()
+    res_off, res_n = cfg.residual_map()
+    entries = make_history(cfg, "cuda")
+    hist = cheb.ResidualHistory(cfg.n_hist, res_off, res_n)
+    for x, e in zip(cfg.nodes, entries):
+        hist.push(x, split_segments(e, cfg))
+    # the reduction alone: one entry against the oracle with w = [1]
+    lay = cheb.cheb_cache_layout(1, cheb.CHEB_BF16, cfg.seg_numel)
+    seg_off = [int(o) for o in lay["seg_offset"]]
+    red = hist.cache.entry(cfg.n_hist - 1)[:res_n].cpu().numpy()
+    exp1, mag1 = oracle.residual([to_host_bits(entries[-1])], [1.0], seg_off, cfg.seg_numel,
+                                 res_off, res_n)
+    _check(red, exp1, mag1, RES_TOL, "push-time reduction")
+    x_in = _x_in(res_n, 11)
+    for t in cfg.targets:
+        x_out = torch.empty_like(x_in)
+        hist.predict(t, x_out, x_in)
+        torch.cuda.synchronize()
+        exp, mag = oracle.residual([to_host_bits(e) for e in entries],
+                                   oracle.weights_row(cfg.nodes, t), seg_off, cfg.seg_numel,
+                                   res_off, res_n, x_in=x_in.cpu().numpy())
+        _check(x_out.cpu().numpy(), exp, mag, COLLAPSED_TOL, f"collapsed t={t}")
+    hist.close()
+
+
+def _compact_problem(cfg, entries, res_off, res_n, seg_off, idx):
+    """Sampled residual elements idx: per segment, the source value each
+    sampled element receives (zero where the segment does not cover it), so
+    the oracle evaluates the same sum on a compact layout."""
+    m = idx.size
+    cols = []
+    for s, (so, sn, ro) in enumerate(zip(seg_off, cfg.seg_numel, res_off)):
+        src = np.full(m, -1, dtype=np.int64)
+        if ro >= 0:
+            inside = (idx >= ro) & (idx < ro + sn)
+            src[inside] = so + idx[inside] - ro
+        cols.append(src)
+    compact = []
+    for e in entries:
+        vals = []
+        for src in cols:
+            take = torch.from_numpy(np.where(src >= 0, src, 0)).to("cuda")
+            v = e.index_select(0, take)
+            v = torch.where(torch.from_numpy(src >= 0).to("cuda"), v, torch.zeros_like(v))
+            vals.append(v)
+        compact.append(to_host_bits(torch.cat(vals)))
+    n_seg = len(cols)
+    return compact, [s * m for s in range(n_seg)], [m] * n_seg, [0] * n_seg, m
+
+
+@pytest.mark.parametrize("cfg", CONFIGS[1:], ids=lambda c: c.name)
+def test_residual_full_size_sampled(cfg):
+    res_off, res_n = cfg.residual_map()
+    entries, cache = _fill(cfg, cfg.nodes)
+    t = cfg.targets[0]
+    w = cheb.cheb_precompute_weights(cache.history(), [t])[0]
+    x_in = _x_in(res_n, 5)
+    x_out = torch.empty_like(x_in)
+    say(f"residual {cfg.name} full size: {len(cfg.segments)} segments, residual {res_n}")
+    cache.residual_apply(w, res_off, x_out, x_in)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(cfg.seed)
+    idx = np.unique(np.concatenate([rng.integers(0, res_n, 20000), np.arange(64),
+                                    np.arange(res_n - 64, res_n)]))
+    comp, so, sn, ro, m = _compact_problem(cfg, entries, res_off, res_n, cache.seg_offset, idx)
+    exp, mag = oracle.residual(comp, oracle.weights_row(cfg.nodes, t), so, sn, ro, m,
+                               x_in=x_in.cpu().numpy()[idx])
+    _check(x_out.cpu().numpy()[idx], exp, mag, RES_TOL, f"{cfg.name} sampled")
+    cache.close()
+    del entries
+    torch.cuda.empty_cache()

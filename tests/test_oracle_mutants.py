@@ -5,6 +5,8 @@ sign, a dropped term, a transposed or shifted index, a wrong rounding rule),
 builds it with gcc into a temporary library, points the oracle's Python
 binding at it and runs the pin battery of ``test_oracle_pins``; at least one
 pin must fail.  All on the CPU; the real oracle is restored afterwards.
+Planted mistakes keep every access in bounds, so a mutant fails a pin
+rather than the process.
 """
 import functools
 import os
@@ -47,6 +49,11 @@ MUTANTS = [
     ("table keeps oldest", "for (int j = 1; j < n; ++j) hist[j - 1] = hist[j];",
      "for (int j = 1; j < n - 1; ++j) hist[j] = hist[j + 1];", 0),
     ("table ignores short-history policy", "(count < n && policy == 0)", "(count < n && policy == 1)", 0),
+    ("residual drops x_in", "x_out[j] = x_in ? x_in[j] : 0.0;\n    if (absmag) absmag[j] = x_in ? fabs",
+     "x_out[j] = 0.0;\n    if (absmag) absmag[j] = x_in ? fabs", 0),
+    ("residual shifted target", "x_out[res_offset[s] + e] += acc;", "x_out[res_offset[s] + (e > 0 ? e - 1 : e)] += acc;", 0),
+    ("residual magnitude drops x_in", "if (absmag) absmag[j] = x_in ? fabs(x_in[j]) : 0.0;\n  }\n  for (int s = 0; s < n_segs; ++s) {\n    if (res_offset[s] < 0) continue;\n#pragma omp parallel for schedule(static)\n    for (int64_t e = 0; e < seg_numel[s]; ++e) {\n      double acc = 0.0, mag = 0.0;\n      for (int k = 0; k < n; ++k) {\n        double f = oracle_bf16",
+     "if (absmag) absmag[j] = 0.0;\n  }\n  for (int s = 0; s < n_segs; ++s) {\n    if (res_offset[s] < 0) continue;\n#pragma omp parallel for schedule(static)\n    for (int64_t e = 0; e < seg_numel[s]; ++e) {\n      double acc = 0.0, mag = 0.0;\n      for (int k = 0; k < n; ++k) {\n        double f = oracle_bf16", 0),
     ("table uses step not abscissa", "return oracle_weights_row(x, count, abscissa[s], w);",
      "return oracle_weights_row(x, count, abscissa[s] + 1.0, w);", 0),
 ]

@@ -375,3 +375,62 @@ def test_table_rows_golden():
                 assert np.allclose(w, [float(e) for e in exact], rtol=0, atol=1e-12 * max(1, np.abs(w).sum()))
         n_cases += 1
     assert n_cases == 5
+
+
+# --------------------------------------------------------------------------
+# Residual application
+# --------------------------------------------------------------------------
+
+def _bf16_bits(vals):
+    return torch.tensor(vals, dtype=torch.float32).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+
+
+def test_residual_hand_worked():
+    """Two entries (w = [-1, 2]), a 4-element residual, three segments: the
+    first adds everywhere, the second into elements 2..3, the third is not
+    added.  Worked by hand from x_{l+1} = x_l + (module outputs)."""
+    F0 = _bf16_bits([1, 2, 3, 4, 5, 6, 7, 8])
+    F1 = _bf16_bits([1, 1, 1, 1, 2, 2, 2, 2])
+    out, mag = oracle.residual([F0, F1], [-1.0, 2.0], slot_offset=[0, 4, 6],
+                               seg_numel=[4, 2, 2], res_offset=[0, 2, -1], res_numel=4,
+                               x_in=[10.0, 20.0, 30.0, 40.0])
+    assert out.tolist() == [11.0, 20.0, 28.0, 36.0]
+    assert mag.tolist() == [13.0, 24.0, 44.0, 56.0]
+
+
+def test_residual_single_segment_is_the_prediction():
+    rng = np.random.default_rng(37)
+    E = 5000
+    F = [_bf16_bits(rng.standard_normal(E)) for _ in range(5)]
+    w = oracle.weights_row([900, 820, 740, 660, 580], 560)
+    out, mag = oracle.residual(F, w, [0], [E], [0], E)
+    ref, rmag = oracle.extrapolate_bf16(F, w)
+    np.testing.assert_array_equal(out, ref)
+    np.testing.assert_array_equal(mag, rmag)
+
+
+def test_residual_blocks_sum_and_order():
+    """DiT-like mapping (every segment adds into the whole residual): the
+    result is x_in plus the sum of the per-segment predictions, whatever the
+    segment order; x_in enters linearly."""
+    rng = np.random.default_rng(41)
+    L, nseg, n = 777, 6, 4
+    F = [_bf16_bits(rng.standard_normal(L * nseg)) for _ in range(n)]
+    w = oracle.weights_row([999, 979, 959, 939], 919)
+    so = np.arange(nseg) * L
+    x_in = rng.standard_normal(L)
+    out, _ = oracle.residual(F, w, so, [L] * nseg, [0] * nseg, L, x_in=x_in)
+    parts = [oracle.extrapolate_bf16([f[o:o + L] for f in F], w, want_absmag=False) for o in so]
+    ref = x_in + np.sum(parts, axis=0)
+    assert np.max(np.abs(out - ref)) <= 1e-12 * (1 + np.max(np.abs(ref)))
+    p = rng.permutation(nseg)
+    out2, _ = oracle.residual(F, w, so[p], [L] * nseg, [0] * nseg, L, x_in=x_in)
+    assert np.max(np.abs(out2 - out)) <= 1e-12 * (1 + np.max(np.abs(ref)))
+    out0, _ = oracle.residual(F, w, so, [L] * nseg, [0] * nseg, L)
+    assert np.max(np.abs((out - out0) - x_in)) <= 1e-12 * (1 + np.max(np.abs(ref)))
+
+
+def test_residual_rejects_segment_outside():
+    F = [_bf16_bits([1.0] * 8)]
+    with pytest.raises(oracle.OracleError):
+        oracle.residual(F, [1.0], [0], [8], [1], 8)
