@@ -103,6 +103,30 @@ CHEB_API int cheb_precompute_weights(const double *hist_t, int32_t n_hist,
                             const double *target_t, int32_t n_target,
                             double *w_out);
 
+/* Weight variants for cheb_precompute_weights_variant. */
+enum {
+  CHEB_RHO_GENERAL = 0,     /* rho_j = 1/omega'(x_j) (Appendix A): the
+                               Lagrange interpolant, as cheb_precompute_weights */
+  CHEB_RHO_ALTERNATING = 1  /* rho_j = (-1)^j (1/2 at both ends, else 1), the
+                               weights printed in Section 3.2: exact for
+                               Chebyshev extrema, a rational interpolant that
+                               reproduces degree <= 1 at equispaced nodes */
+};
+
+/* cheb_precompute_weights with a choice of barycentric weights rho_j in the
+ * coefficient equation of Section 3.2.  Arguments and errors as
+ * cheb_precompute_weights, plus CHEB_E_INVAL for an unknown variant. */
+CHEB_API int cheb_precompute_weights_variant(const double *hist_t, int32_t n_hist,
+                                             const double *target_t, int32_t n_target,
+                                             int32_t variant, double *w_out);
+
+/* Chebyshev points on [a, b], largest first, for schedules that place full
+ * steps at them: kind 1 the roots cos((2j-1) pi / 2n), j = 1..n (Section
+ * 3.2, node equation); kind 2 the extrema cos((j-1) pi / (n-1)) (n >= 2).
+ *   x_out [n] host fp64.  1 <= n <= CHEB_MAX_NODES.
+ * Errors: CHEB_E_INVAL, CHEB_E_NONFINITE. */
+CHEB_API int cheb_chebyshev_nodes(int32_t n, int32_t kind, double a, double b, double *x_out);
+
 /* ------------------------------------------------------------------------ */
 /* Stateless combination.                                                    */
 /* ------------------------------------------------------------------------ */
@@ -287,6 +311,13 @@ typedef struct cheb_table cheb_table;
  * Errors: CHEB_E_INVAL, CHEB_E_NONFINITE, CHEB_E_DUPNODE. */
 CHEB_API int cheb_table_build(cheb_table **out, int32_t T, int32_t s0, int32_t s1, int32_t r,
                               int32_t n_hist, const double *abscissa, int32_t policy);
+
+/* The same for an arbitrary set of full steps (for example steps placed at
+ * rounded Chebyshev points, cheb_chebyshev_nodes, instead of on the grid
+ * F): is_full [T] host, nonzero where the step runs the network.  The
+ * table records r = 0 (no grid).  Errors: as cheb_table_build. */
+CHEB_API int cheb_table_build_mask(cheb_table **out, int32_t T, const uint8_t *is_full,
+                                   int32_t n_hist, const double *abscissa, int32_t policy);
 
 /* Frees the table.  NULL is accepted. */
 CHEB_API int cheb_table_destroy(cheb_table *t);

@@ -77,6 +77,10 @@ def bind(path):
     L.oracle_extrapolate_f64.restype = None
     L.oracle_full_schedule.argtypes = [ctypes.c_int] * 4 + [
         ctypes.POINTER(ctypes.c_uint8)]
+    L.oracle_chebyshev_nodes.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_double,
+                                         ctypes.c_double, _c_double_p]
+    L.oracle_weights_row_alternating.argtypes = [_c_double_p, ctypes.c_int, ctypes.c_double,
+                                                 _c_double_p]
     _i64 = ctypes.POINTER(ctypes.c_int64)
     L.oracle_residual_bf16.argtypes = [ctypes.POINTER(_c_u16_p), ctypes.c_int, _c_double_p,
                                        _i64, _i64, _i64, ctypes.c_int, _c_double_p,
@@ -85,6 +89,9 @@ def bind(path):
                                       _i64, _i64, _i64, ctypes.c_int, _c_double_p,
                                       ctypes.c_int64, _c_double_p, _c_double_p]
     _ip = ctypes.POINTER(ctypes.c_int)
+    L.oracle_table_row_mask.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_uint8), ctypes.c_int,
+                                        _c_double_p, ctypes.c_int, ctypes.c_int, _ip, _ip, _ip,
+                                        _c_double_p]
     L.oracle_table_row.argtypes = [ctypes.c_int] * 5 + [_c_double_p, ctypes.c_int, ctypes.c_int,
                                                         _ip, _ip, _ip, _c_double_p]
     return L
@@ -262,6 +269,25 @@ def parity_error(got, expect, absmag, floor=1e-3):
             normwise, float(np.mean(floored)))
 
 
+def table_row_mask(full_mask, n, abscissa, policy, step):
+    """table_row for an arbitrary full-step mask."""
+    mask = np.ascontiguousarray(full_mask, dtype=np.uint8)
+    x = _f64(abscissa)
+    T = mask.size
+    if x.size != T:
+        raise OracleError("one abscissa per step")
+    kind, n_used = ctypes.c_int(), ctypes.c_int()
+    nodes = (ctypes.c_int * 64)()
+    w = np.zeros(64, dtype=np.float64)
+    rc = lib().oracle_table_row_mask(T, mask.ctypes.data_as(ctypes.POINTER(ctypes.c_uint8)), int(n),
+                                     _ptr(x, ctypes.c_double), int(policy), int(step),
+                                     ctypes.byref(kind), ctypes.byref(n_used), nodes,
+                                     _ptr(w, ctypes.c_double))
+    if rc != 0:
+        raise OracleError(_NODE_ERRORS.get(rc, f"oracle error {rc}"))
+    return kind.value, [nodes[j] for j in range(n_used.value)], w[:n_used.value].copy()
+
+
 def table_row(T, s0, s1, r, n, abscissa, policy, step):
     """(kind, node steps, weights) of `step` by simulating Algorithm 1:
     kind 0 = full step, 1 = predicted from the listed entries."""
@@ -310,3 +336,21 @@ def residual(slots, w, slot_offset, seg_numel, res_offset, res_numel, x_in=None,
     if rc != 0:
         raise OracleError("segment outside the residual")
     return out, mag
+
+
+def chebyshev_nodes(n, kind=1, a=-1.0, b=1.0):
+    """Chebyshev roots (kind 1) or extrema (kind 2) on [a, b], largest first."""
+    x = np.empty(int(n), dtype=np.float64)
+    if lib().oracle_chebyshev_nodes(int(n), int(kind), float(a), float(b),
+                                    _ptr(x, ctypes.c_double)) != 0:
+        raise OracleError("bad Chebyshev node request")
+    return x
+
+
+def weights_row_alternating(x, xstar):
+    """Coefficients from the alternating weights printed in Section 3.2."""
+    x = _f64(x)
+    w = np.empty_like(x)
+    _check(lib().oracle_weights_row_alternating(_ptr(x, ctypes.c_double), len(x), float(xstar),
+                                                _ptr(w, ctypes.c_double)))
+    return w

@@ -288,7 +288,8 @@ int oracle_full_schedule(int T, int s0, int s1, int r, uint8_t *is_full) {
 /* Offline table by simulating the online stage (Algorithm 1).               */
 /* ------------------------------------------------------------------------ */
 
-/* What step `step` does under schedule (T, s0, s1, r) with history size n,
+/* What step `step` does under a full-step mask full[0..T-1] (or, in
+ * oracle_table_row, under the schedule (T, s0, s1, r)) with history size n,
  * found by running Algorithm 1's loop from step 0: a full step appends
  * itself to the history H (dropping the oldest once H holds n entries); a
  * skipped step with |H| = n gets the coefficients of the abscissae of H at
@@ -299,14 +300,11 @@ int oracle_full_schedule(int T, int s0, int s1, int r, uint8_t *is_full) {
  *   *n_used   entries the prediction uses (0 for a full step)
  *   nodes[]   their steps, oldest to newest;  w[] their coefficients.
  * Returns 0, or a negative code (bad arguments, or oracle_weights_row's). */
-int oracle_table_row(int T, int s0, int s1, int r, int n, const double *abscissa,
-                     int policy, int step, int *kind, int *n_used, int *nodes,
-                     double *w) {
-  if (n < 1 || n > ORACLE_MAX_NODES || step < 0 || step >= T) return -1;
+int oracle_table_row_mask(int T, const uint8_t *full, int n, const double *abscissa,
+                          int policy, int step, int *kind, int *n_used, int *nodes,
+                          double *w) {
+  if (T < 1 || n < 1 || n > ORACLE_MAX_NODES || step < 0 || step >= T) return -1;
   if (policy != 0 && policy != 1) return -1;
-  uint8_t full[4096];
-  if (T > 4096) return -1;
-  if (oracle_full_schedule(T, s0, s1, r, full) < 0) return -1;
   int hist[ORACLE_MAX_NODES];
   int count = 0;
   for (int s = 0; s <= step; ++s) {
@@ -335,6 +333,15 @@ int oracle_table_row(int T, int s0, int s1, int r, int n, const double *abscissa
     }
   }
   return -1; /* not reached */
+}
+
+int oracle_table_row(int T, int s0, int s1, int r, int n, const double *abscissa,
+                     int policy, int step, int *kind, int *n_used, int *nodes,
+                     double *w) {
+  uint8_t full[4096];
+  if (T < 1 || T > 4096) return -1;
+  if (oracle_full_schedule(T, s0, s1, r, full) < 0) return -1;
+  return oracle_table_row_mask(T, full, n, abscissa, policy, step, kind, n_used, nodes, w);
 }
 
 /* ------------------------------------------------------------------------ */
@@ -405,5 +412,51 @@ int oracle_residual_f32(const float *const *F, int n, const double *w,
       if (absmag) absmag[res_offset[s] + e] += mag;
     }
   }
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Node and weight variants (Section 3.2).                                    */
+/* ------------------------------------------------------------------------ */
+
+/* Chebyshev points on [a, b], largest first.  kind 1: the roots of T_n,
+ * cos((2j-1) pi / (2n)), j = 1..n (Section 3.2, node equation); kind 2: the
+ * extrema cos((j-1) pi / (n-1)), j = 1..n (n >= 2).  Returns 0 or -1. */
+int oracle_chebyshev_nodes(int n, int kind, double a, double b, double *x) {
+  if (n < 1 || (kind != 1 && kind != 2) || (kind == 2 && n < 2)) return -1;
+  const double pi = 3.14159265358979323846;
+  for (int j = 1; j <= n; ++j) {
+    double c = (kind == 1) ? cos((2.0 * j - 1.0) * pi / (2.0 * n))
+                           : cos((j - 1.0) * pi / (n - 1.0));
+    x[j - 1] = 0.5 * (a + b) + 0.5 * (b - a) * c;
+  }
+  return 0;
+}
+
+/* Coefficients from the alternating weights printed in Section 3.2,
+ * rho_j = (-1)^j * (1/2 at j = 1 and j = n, 1 otherwise), put into the
+ * coefficient equation of Section 3.2 at the given nodes.  A target on a
+ * node gets that node's unit row.  Returns 0 or the node-check code. */
+int oracle_weights_row_alternating(const double *x, int n, double xstar, double *w) {
+  int rc = oracle_check_nodes(x, n);
+  if (rc) return rc;
+  if (!isfinite(xstar)) return -2;
+  for (int j = 0; j < n; ++j) {
+    if (xstar == x[j]) {
+      for (int k = 0; k < n; ++k) w[k] = (k == j) ? 1.0 : 0.0;
+      return 0;
+    }
+  }
+  if (n == 1) {
+    w[0] = 1.0;
+    return 0;
+  }
+  double denom = 0.0;
+  for (int j = 0; j < n; ++j) {
+    double rho = ((j % 2) ? -1.0 : 1.0) * ((j == 0 || j == n - 1) ? 0.5 : 1.0);
+    w[j] = rho / (xstar - x[j]);
+    denom += w[j];
+  }
+  for (int j = 0; j < n; ++j) w[j] /= denom;
   return 0;
 }

@@ -42,10 +42,15 @@ void oracle_extrapolate_f64(const double *const *F, int n, const double *w,
                             int64_t count, double *out);
 
 int oracle_full_schedule(int T, int s0, int s1, int r, uint8_t *is_full);
+int oracle_table_row_mask(int T, const uint8_t *full, int n, const double *abscissa,
+                          int policy, int step, int *kind, int *n_used, int *nodes,
+                          double *w);
 int oracle_table_row(int T, int s0, int s1, int r, int n, const double *abscissa,
                      int policy, int step, int *kind, int *n_used, int *nodes,
                      double *w);
 
+int oracle_chebyshev_nodes(int n, int kind, double a, double b, double *x);
+int oracle_weights_row_alternating(const double *x, int n, double xstar, double *w);
 int oracle_residual_bf16(const uint16_t *const *F, int n, const double *w,
                          const int64_t *slot_offset, const int64_t *seg_numel,
                          const int64_t *res_offset, int n_segs, const double *x_in,

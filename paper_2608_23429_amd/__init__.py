@@ -13,15 +13,16 @@ import numpy as np
 import torch
 
 from ._binding import (  # noqa: F401  (re-exported C entry points)
-    CHEB_BF16, CHEB_F32, CHEB_MAX_NODES, CHEB_MAX_OUTPUTS, CHEB_MAX_SLOTS, CHEB_SHORT_FULL,
-    CHEB_SHORT_LOWER, ChebError,
+    CHEB_BF16, CHEB_F32, CHEB_MAX_NODES, CHEB_MAX_OUTPUTS, CHEB_MAX_SLOTS, CHEB_RHO_ALTERNATING,
+    CHEB_RHO_GENERAL, CHEB_SHORT_FULL, CHEB_SHORT_LOWER, ChebError, cheb_chebyshev_nodes,
+    cheb_precompute_weights_variant,
     cheb_cache_begin_push, cheb_cache_commit, cheb_cache_create, cheb_cache_destroy,
     cheb_cache_dtype, cheb_cache_entry, cheb_cache_history, cheb_cache_layout, cheb_cache_push,
     cheb_cache_reset, cheb_cache_segment_offset, cheb_cache_slot_numel, cheb_combine,
     cheb_combine_multi, cheb_extrapolate, cheb_extrapolate_at, cheb_extrapolate_at_multi,
     cheb_extrapolate_multi, cheb_extrapolate_steps, cheb_get_launch_config, cheb_last_error,
     cheb_precompute_weights, cheb_residual_apply, cheb_residual_reduce, cheb_schedule,
-    cheb_set_launch_config, cheb_table_build,
+    cheb_set_launch_config, cheb_table_build, cheb_table_build_mask,
     cheb_table_destroy, cheb_table_info, cheb_table_load, cheb_table_save, cheb_table_step,
     cheb_version,
 )
@@ -101,6 +102,10 @@ class ChebTable:
         info = cheb_table_info(self._h)
         self.T, self.n_hist, self.policy, self.n_full = (
             info["T"], info["n_hist"], info["policy"], info["n_full"])
+
+    @classmethod
+    def from_mask(cls, is_full, n_hist, abscissa, policy=CHEB_SHORT_FULL):
+        return cls(_handle=cheb_table_build_mask(is_full, n_hist, abscissa, policy))
 
     @classmethod
     def load(cls, path):

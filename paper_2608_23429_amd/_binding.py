@@ -26,6 +26,9 @@ CHEB_E_IO = -9
 CHEB_SHORT_FULL = 0
 CHEB_SHORT_LOWER = 1
 
+CHEB_RHO_GENERAL = 0
+CHEB_RHO_ALTERNATING = 1
+
 CHEB_BF16 = 0
 CHEB_F32 = 1
 CHEB_MAX_SLOTS = 8
@@ -65,6 +68,10 @@ SIGNATURES = {
     "cheb_last_error": [],
     "cheb_version": [],
     "cheb_precompute_weights": [_dp, ctypes.c_int32, _dp, ctypes.c_int32, _dp],
+    "cheb_precompute_weights_variant": [_dp, ctypes.c_int32, _dp, ctypes.c_int32,
+                                        ctypes.c_int32, _dp],
+    "cheb_chebyshev_nodes": [ctypes.c_int32, ctypes.c_int32, ctypes.c_double, ctypes.c_double,
+                             _dp],
     "cheb_combine": [_vpp, ctypes.c_int32, _dp, _vp, ctypes.c_int64, ctypes.c_int32, _vp],
     "cheb_combine_multi": [_vpp, ctypes.c_int32, _dp, ctypes.c_int32, _vpp, ctypes.c_int64,
                            ctypes.c_int32, _vp],
@@ -84,6 +91,8 @@ SIGNATURES = {
     "cheb_cache_dtype": [_vp, _i32p],
     "cheb_schedule": [ctypes.c_int32] * 4 + [ctypes.POINTER(ctypes.c_uint8)],
     "cheb_table_build": [ctypes.POINTER(_vp)] + [ctypes.c_int32] * 5 + [_dp, ctypes.c_int32],
+    "cheb_table_build_mask": [ctypes.POINTER(_vp), ctypes.c_int32, ctypes.POINTER(ctypes.c_uint8),
+                              ctypes.c_int32, _dp, ctypes.c_int32],
     "cheb_table_destroy": [_vp],
     "cheb_table_info": [_vp, _i32p, _i32p, _i32p, _i32p],
     "cheb_table_step": [_vp, ctypes.c_int32, _i32p, _i32p, _i32p, _dp],
@@ -151,6 +160,21 @@ def cheb_precompute_weights(hist_t, target_t) -> np.ndarray:
     _check(LIB.cheb_precompute_weights(_dptr(h), h.size, _dptr(t) if t.size else None,
                                        t.size, _dptr(w) if w.size else None))
     return w
+
+
+def cheb_precompute_weights_variant(hist_t, target_t, variant=CHEB_RHO_GENERAL) -> np.ndarray:
+    h = _f64(hist_t).reshape(-1)
+    t = _f64(target_t).reshape(-1)
+    w = np.empty((t.size, h.size), dtype=np.float64)
+    _check(LIB.cheb_precompute_weights_variant(_dptr(h), h.size, _dptr(t) if t.size else None,
+                                               t.size, int(variant), _dptr(w) if w.size else None))
+    return w
+
+
+def cheb_chebyshev_nodes(n, kind=1, a=-1.0, b=1.0) -> np.ndarray:
+    x = np.empty(int(n), dtype=np.float64)
+    _check(LIB.cheb_chebyshev_nodes(int(n), int(kind), float(a), float(b), _dptr(x)))
+    return x
 
 
 def cheb_combine(src_ptrs, w, out_ptr, numel, dtype, stream=0):
@@ -259,6 +283,16 @@ def cheb_table_build(T, s0, s1, r, n_hist, abscissa, policy=CHEB_SHORT_FULL):
     h = ctypes.c_void_p()
     _check(LIB.cheb_table_build(ctypes.byref(h), int(T), int(s0), int(s1), int(r), int(n_hist),
                                 _dptr(x), int(policy)))
+    return h
+
+
+def cheb_table_build_mask(is_full, n_hist, abscissa, policy=CHEB_SHORT_FULL):
+    mask = np.ascontiguousarray(is_full, dtype=np.uint8).reshape(-1)
+    x = _f64(abscissa).reshape(-1)
+    h = ctypes.c_void_p()
+    _check(LIB.cheb_table_build_mask(ctypes.byref(h), mask.size,
+                                     mask.ctypes.data_as(ctypes.POINTER(ctypes.c_uint8)),
+                                     int(n_hist), _dptr(x), int(policy)))
     return h
 
 

@@ -118,6 +118,37 @@ int weights_row(const double *x, int n, double target, double *w) {
   return CHEB_OK;
 }
 
+// Coefficients from the alternating weights printed in Section 3.2,
+// rho_j = (-1)^j (1/2 at the first and last node, 1 otherwise), in the
+// coefficient equation.  They are the barycentric weights of Chebyshev
+// extrema; at other nodes they give a rational interpolant.
+int weights_row_alternating(const double *x, int n, double target, double *w) {
+  if (n < 1 || n > CHEB_MAX_NODES)
+    return fail(CHEB_E_INVAL, "history size %d outside 1..%d", n, CHEB_MAX_NODES);
+  if (!isfinite(target)) return fail(CHEB_E_NONFINITE, "target abscissa is not finite");
+  for (int j = 0; j < n; ++j) {
+    if (!isfinite(x[j])) return fail(CHEB_E_NONFINITE, "history abscissa %d is not finite", j);
+    for (int k = 0; k < j; ++k)
+      if (x[j] == x[k])
+        return fail(CHEB_E_DUPNODE, "history abscissae %d and %d are equal (%.17g)", k, j, x[j]);
+  }
+  for (int j = 0; j < n; ++j) {
+    if (target == x[j]) {
+      for (int k = 0; k < n; ++k) w[k] = (k == j) ? 1.0 : 0.0;
+      return CHEB_OK;
+    }
+  }
+  double total = 0.0;
+  for (int j = 0; j < n; ++j) {
+    const double sign = (j & 1) ? -1.0 : 1.0;
+    const double end = (n > 1 && (j == 0 || j == n - 1)) ? 0.5 : 1.0;
+    w[j] = sign * end / (target - x[j]);
+    total += w[j];
+  }
+  for (int j = 0; j < n; ++j) w[j] /= total;
+  return CHEB_OK;
+}
+
 }  // namespace cheb
 
 using namespace cheb;
@@ -172,6 +203,45 @@ int cheb_precompute_weights(const double *hist_t, int32_t n_hist, const double *
   for (int32_t m = 0; m < n_target; ++m) {
     weights_row(hist_t, n_hist, target_t[m], row);
     memcpy(w_out + size_t(m) * n_hist, row, sizeof(double) * n_hist);
+  }
+  return ok();
+}
+
+int cheb_precompute_weights_variant(const double *hist_t, int32_t n_hist,
+                                    const double *target_t, int32_t n_target, int32_t variant,
+                                    double *w_out) {
+  if (variant == CHEB_RHO_GENERAL)
+    return cheb_precompute_weights(hist_t, n_hist, target_t, n_target, w_out);
+  if (variant != CHEB_RHO_ALTERNATING) return fail(CHEB_E_INVAL, "unknown weight variant %d", variant);
+  if (!hist_t) return fail(CHEB_E_INVAL, "hist_t is NULL");
+  if (n_target < 0) return fail(CHEB_E_INVAL, "n_target is negative");
+  if (n_target > 0 && (!target_t || !w_out)) return fail(CHEB_E_INVAL, "target_t or w_out is NULL");
+  double row[CHEB_MAX_NODES];
+  for (int32_t m = 0; m < n_target; ++m) {
+    int rc = weights_row_alternating(hist_t, n_hist, target_t[m], row);
+    if (rc != CHEB_OK) return rc;
+  }
+  if (n_target == 0) {
+    int rc = weights_row_alternating(hist_t, n_hist, hist_t[0], row);
+    if (rc != CHEB_OK) return rc;
+  }
+  for (int32_t m = 0; m < n_target; ++m) {
+    weights_row_alternating(hist_t, n_hist, target_t[m], row);
+    memcpy(w_out + size_t(m) * n_hist, row, sizeof(double) * n_hist);
+  }
+  return ok();
+}
+
+int cheb_chebyshev_nodes(int32_t n, int32_t kind, double a, double b, double *x_out) {
+  if (!x_out) return fail(CHEB_E_INVAL, "x_out is NULL");
+  if (n < 1 || n > CHEB_MAX_NODES) return fail(CHEB_E_INVAL, "n %d outside 1..%d", n, CHEB_MAX_NODES);
+  if (kind != 1 && kind != 2) return fail(CHEB_E_INVAL, "kind must be 1 or 2");
+  if (kind == 2 && n < 2) return fail(CHEB_E_INVAL, "Chebyshev extrema need n >= 2");
+  if (!isfinite(a) || !isfinite(b)) return fail(CHEB_E_NONFINITE, "interval is not finite");
+  const double mid = 0.5 * (a + b), half = 0.5 * (b - a);
+  for (int32_t j = 0; j < n; ++j) {
+    const double angle = kind == 1 ? M_PI * (2.0 * j + 1.0) / (2.0 * n) : M_PI * j / (n - 1.0);
+    x_out[j] = mid + half * cos(angle);
   }
   return ok();
 }

@@ -43,7 +43,8 @@ bool in_schedule(int32_t T, int32_t s0, int32_t s1, int32_t r, int32_t s) {
   return (s - s0) % r == 0;
 }
 
-int fill_rows(cheb_table *t) {
+// Rows of every step given which steps the schedule runs in full.
+int fill_rows(cheb_table *t, const uint8_t *scheduled) {
   const int32_t T = t->T, n = t->n_hist;
   t->predicted.assign(size_t(T), 0);
   t->n_used.assign(size_t(T), 0);
@@ -54,8 +55,7 @@ int fill_rows(cheb_table *t) {
   std::vector<int32_t> full_steps;
   for (int32_t s = 0; s < T; ++s) {
     const int32_t have = int32_t(full_steps.size());
-    const bool runs = in_schedule(T, t->s0, t->s1, t->r, s) || have == 0 ||
-                      (t->policy == 0 && have < n);
+    const bool runs = scheduled[s] || have == 0 || (t->policy == 0 && have < n);
     if (runs) full_steps.push_back(s);
   }
   double x[CHEB_MAX_NODES];
@@ -111,7 +111,42 @@ int cheb_table_build(cheb_table **out, int32_t T, int32_t s0, int32_t s1, int32_
   t->n_hist = n_hist;
   t->policy = policy;
   t->abscissa.assign(abscissa, abscissa + T);
-  int rc = fill_rows(t);
+  std::vector<uint8_t> scheduled(static_cast<size_t>(T), 0);
+  for (int32_t s = 0; s < T; ++s) scheduled[size_t(s)] = in_schedule(T, s0, s1, r, s) ? 1 : 0;
+  int rc = fill_rows(t, scheduled.data());
+  if (rc != CHEB_OK) {
+    delete t;
+    return rc;
+  }
+  *out = t;
+  return ok();
+}
+
+int cheb_table_build_mask(cheb_table **out, int32_t T, const uint8_t *is_full, int32_t n_hist,
+                          const double *abscissa, int32_t policy) {
+  if (!out) return fail(CHEB_E_INVAL, "out is NULL");
+  *out = nullptr;
+  if (T < 1 || T > kMaxSteps) return fail(CHEB_E_INVAL, "T %d outside 1..%d", T, kMaxSteps);
+  if (!is_full || !abscissa) return fail(CHEB_E_INVAL, "is_full or abscissa is NULL");
+  if (n_hist < 1 || n_hist > CHEB_MAX_SLOTS)
+    return fail(CHEB_E_INVAL, "n_hist %d outside 1..%d", n_hist, CHEB_MAX_SLOTS);
+  if (policy != CHEB_SHORT_FULL && policy != CHEB_SHORT_LOWER)
+    return fail(CHEB_E_INVAL, "unknown short-history policy %d", policy);
+  for (int32_t s = 0; s < T; ++s)
+    if (!isfinite(abscissa[s])) return fail(CHEB_E_NONFINITE, "abscissa of step %d", s);
+  cheb_table *t = new (std::nothrow) cheb_table();
+  if (!t) return fail(CHEB_E_INVAL, "out of host memory");
+  // A mask table records no (s0, s1, r); saved tables carry r = 0 to say so.
+  t->T = T;
+  t->s0 = 0;
+  t->s1 = 0;
+  t->r = 0;
+  t->n_hist = n_hist;
+  t->policy = policy;
+  t->abscissa.assign(abscissa, abscissa + T);
+  std::vector<uint8_t> scheduled(is_full, is_full + T);
+  for (uint8_t &v : scheduled) v = v ? 1 : 0;
+  int rc = fill_rows(t, scheduled.data());
   if (rc != CHEB_OK) {
     delete t;
     return rc;
@@ -196,7 +231,9 @@ int cheb_table_load(cheb_table **out, const char *path) {
   if (fscanf(f, " T %d s0 %d s1 %d r %d n_hist %d policy %d", &tmp.T, &tmp.s0, &tmp.s1,
              &tmp.r, &tmp.n_hist, &tmp.policy) != 6)
     return bad("parameters");
-  if (!schedule_args_ok(tmp.T, tmp.s0, tmp.s1, tmp.r) || tmp.n_hist < 1 ||
+  const bool mask_table = tmp.r == 0 && tmp.s0 == 0 && tmp.s1 == 0;
+  if ((!mask_table && !schedule_args_ok(tmp.T, tmp.s0, tmp.s1, tmp.r)) ||
+      (mask_table && (tmp.T < 1 || tmp.T > kMaxSteps)) || tmp.n_hist < 1 ||
       tmp.n_hist > CHEB_MAX_SLOTS || (tmp.policy != 0 && tmp.policy != 1))
     return bad("parameters out of range");
   const int32_t T = tmp.T, n = tmp.n_hist;

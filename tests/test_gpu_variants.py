@@ -1,0 +1,60 @@
+"""Weight variants on the device path: the same kernel with the alternating
+weights printed in Section 3.2, and a table whose full steps sit at rounded
+Chebyshev points, against the oracle."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_23429_amd as cheb
+from synth import CONFIGS, make_history, split_segments
+from tests.gpu_util import check_parity, to_host_bits
+
+pytestmark = pytest.mark.gpu
+
+
+def test_alternating_weights_through_the_kernel():
+    cfg = CONFIGS[4].shrunk(300_000)
+    entries = make_history(cfg, "cuda")
+    cache = cheb.ChebCache(cfg.n_hist, torch.bfloat16, cfg.seg_numel)
+    for x, e in zip(cfg.nodes, entries):
+        cache.push(x, split_segments(e, cfg))
+    w = cheb.cheb_precompute_weights_variant(cfg.nodes, cfg.targets, cheb.CHEB_RHO_ALTERNATING)
+    outs = cache.extrapolate_multi(w)
+    torch.cuda.synchronize()
+    hosts = [to_host_bits(e) for e in entries]
+    for m, t in enumerate(cfg.targets):
+        check_parity(to_host_bits(outs[m]), hosts, oracle.weights_row_alternating(cfg.nodes, t),
+                     "bf16", f"alternating t={t}")
+    cache.close()
+
+
+def test_chebyshev_placed_full_steps_online():
+    """Full steps at rounded Chebyshev roots of a 50-step flow schedule,
+    predicted steps from the table, each checked against the oracle's
+    Algorithm-1 simulation on the same mask."""
+    cfg = CONFIGS[4].shrunk(100_000)
+    T, n = 50, 4
+    sigma = 1.0 - np.arange(T) / T
+    steps = np.unique(np.rint(cheb.cheb_chebyshev_nodes(14, 1, 0, T - 1)).astype(int))
+    mask = np.zeros(T, dtype=bool)
+    mask[steps] = True
+    table = cheb.ChebTable.from_mask(mask, n, sigma, cheb.CHEB_SHORT_LOWER)
+    full = [s for s in range(T) if not table.step(s)[0]]
+    feats = dict(zip(full, make_history(cfg, "cuda", nodes=sigma[full])))
+    hosts = {s: to_host_bits(f) for s, f in feats.items()}
+    cache = cheb.ChebCache(n, torch.bfloat16, cfg.seg_numel)
+    runs = dict(table.runs())
+    s = 0
+    while s < T:
+        if not table.step(s)[0]:
+            cache.push(sigma[s], split_segments(feats[s], cfg))
+            s += 1
+            continue
+        outs = cache.extrapolate_steps(table, s, runs[s])
+        torch.cuda.synchronize()
+        for m, o in enumerate(outs):
+            kind, nodes, w = oracle.table_row_mask(mask, n, sigma, 1, s + m)
+            check_parity(to_host_bits(o), [hosts[j] for j in nodes], w, "bf16", f"step {s + m}")
+        s += runs[s]
+    cache.close()

@@ -54,6 +54,10 @@ MUTANTS = [
     ("residual shifted target", "x_out[res_offset[s] + e] += acc;", "x_out[res_offset[s] + (e > 0 ? e - 1 : e)] += acc;", 0),
     ("residual magnitude drops x_in", "if (absmag) absmag[j] = x_in ? fabs(x_in[j]) : 0.0;\n  }\n  for (int s = 0; s < n_segs; ++s) {\n    if (res_offset[s] < 0) continue;\n#pragma omp parallel for schedule(static)\n    for (int64_t e = 0; e < seg_numel[s]; ++e) {\n      double acc = 0.0, mag = 0.0;\n      for (int k = 0; k < n; ++k) {\n        double f = oracle_bf16",
      "if (absmag) absmag[j] = 0.0;\n  }\n  for (int s = 0; s < n_segs; ++s) {\n    if (res_offset[s] < 0) continue;\n#pragma omp parallel for schedule(static)\n    for (int64_t e = 0; e < seg_numel[s]; ++e) {\n      double acc = 0.0, mag = 0.0;\n      for (int k = 0; k < n; ++k) {\n        double f = oracle_bf16", 0),
+    ("alternating weights keep end halves off", "((j == 0 || j == n - 1) ? 0.5 : 1.0)",
+     "((j == 0) ? 0.5 : 1.0)", 0),
+    ("alternating weights without sign", "double rho = ((j % 2) ? -1.0 : 1.0)", "double rho = ((j % 2) ? 1.0 : 1.0)", 0),
+    ("Chebyshev roots shifted", "cos((2.0 * j - 1.0) * pi / (2.0 * n))", "cos((2.0 * j) * pi / (2.0 * n))", 0),
     ("table uses step not abscissa", "return oracle_weights_row(x, count, abscissa[s], w);",
      "return oracle_weights_row(x, count, abscissa[s] + 1.0, w);", 0),
 ]

@@ -434,3 +434,67 @@ def test_residual_rejects_segment_outside():
     F = [_bf16_bits([1.0] * 8)]
     with pytest.raises(oracle.OracleError):
         oracle.residual(F, [1.0], [0], [8], [1], 8)
+
+
+# --------------------------------------------------------------------------
+# Node and weight variants (Section 3.2)
+# --------------------------------------------------------------------------
+
+def test_chebyshev_nodes_are_roots_and_extrema():
+    """Kind 1 are the zeros of T_N, kind 2 the points where |T_{N-1}| = 1
+    (checked with numpy's Chebyshev series evaluation)."""
+    for N in range(2, 10):
+        r = oracle.chebyshev_nodes(N, 1)
+        assert np.max(np.abs(np.polynomial.chebyshev.chebval(r, [0] * N + [1]))) < 1e-14
+        e = oracle.chebyshev_nodes(N, 2)
+        assert np.allclose(np.abs(np.polynomial.chebyshev.chebval(e, [0] * (N - 1) + [1])), 1.0,
+                           atol=1e-14)
+        assert np.all(np.diff(r) < 0) and np.all(np.diff(e) < 0)
+    x = oracle.chebyshev_nodes(5, 1, 200.0, 1000.0)
+    assert np.allclose((x - 600.0) / 400.0, oracle.chebyshev_nodes(5, 1))
+
+
+def test_general_weights_at_chebyshev_points_closed_forms():
+    """Textbook closed forms of rho_j = 1/omega'(x_j): at the roots of T_N,
+    proportional to (-1)^j sin((2j-1) pi / 2N); at the extrema, proportional
+    to the alternating weights printed in Section 3.2."""
+    for N in range(2, 10):
+        x = oracle.chebyshev_nodes(N, 1)
+        rho = oracle.barycentric_rho(x)
+        cf = np.array([(-1) ** j * np.sin((2 * j - 1) * np.pi / (2 * N)) for j in range(1, N + 1)])
+        ratio = rho / cf
+        assert np.allclose(ratio, ratio[0], rtol=1e-12)
+        e = oracle.chebyshev_nodes(N, 2)
+        alt = np.array([(-1) ** j * (0.5 if j in (0, N - 1) else 1.0) for j in range(N)])
+        ratio = oracle.barycentric_rho(e) / alt
+        assert np.allclose(ratio, ratio[0], rtol=1e-12)
+        for t in (1.3, -1.7, 0.123):
+            np.testing.assert_allclose(oracle.weights_row_alternating(e, t),
+                                       oracle.weights_row(e, t), rtol=0, atol=_wtol(oracle.weights_row(e, t), 64))
+
+
+def test_alternating_weights_at_equispaced_nodes_reproduce_degree_one_only():
+    """Reading of Section 3.2 against Appendix A: the printed alternating
+    weights at equispaced nodes form a rational interpolant that reproduces
+    constants and straight lines but not quadratics; Appendix A's general
+    weights reproduce every degree up to N-1."""
+    x = np.linspace(-1.0, 1.0, 6)
+    rng = np.random.default_rng(43)
+    for deg, exact in [(0, True), (1, True), (2, False), (3, False)]:
+        c = rng.standard_normal(deg + 1)
+        f = np.polynomial.polynomial.polyval(x, c)
+        for t in (1.2, 1.5):
+            err = abs(oracle.weights_row_alternating(x, t) @ f - np.polynomial.polynomial.polyval(t, c))
+            assert (err < 1e-12) == exact, (deg, t, err)
+            assert abs(oracle.weights_row(x, t) @ f - np.polynomial.polynomial.polyval(t, c)) < 1e-11
+    assert oracle.weights_row_alternating(x, x[2]).tolist() == [0, 0, 1, 0, 0, 0]
+
+
+def test_table_mask_of_schedule_equals_schedule_rows():
+    x = 999.0 - 37.0 * np.arange(20)
+    mask = oracle.full_schedule(20, 2, 1, 4)
+    for policy in (0, 1):
+        for s in range(20):
+            a = oracle.table_row(20, 2, 1, 4, 3, x, policy, s)
+            b = oracle.table_row_mask(mask, 3, x, policy, s)
+            assert a[0] == b[0] and a[1] == b[1] and np.array_equal(a[2], b[2])

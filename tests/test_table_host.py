@@ -168,3 +168,37 @@ def test_extrapolate_steps_checks_ring_against_row():
     assert code(17, out[:3]) == B.CHEB_E_INVAL              # runs past the table
     assert code(7, out[:0]) == B.CHEB_E_INVAL               # no outputs
     cheb.cheb_cache_destroy(h)
+
+
+def test_mask_tables_match_oracle_and_roundtrip(tmp_path):
+    rng = np.random.default_rng(77)
+    for policy in (B.CHEB_SHORT_FULL, B.CHEB_SHORT_LOWER):
+        for _ in range(40):
+            T = int(rng.integers(2, 50))
+            mask = rng.random(T) < rng.uniform(0.1, 0.6)
+            n = int(rng.integers(1, 7))
+            x = np.sort(rng.uniform(0, 1, T))[::-1].copy()
+            t = cheb.ChebTable.from_mask(mask, n, x, policy)
+            for s in range(T):
+                pred, nodes, w = t.step(s)
+                kind, onodes, ow = oracle.table_row_mask(mask, n, x, policy, s)
+                assert pred == bool(kind) and nodes == onodes
+                if pred:
+                    assert np.max(np.abs(w - ow)) <= _wtol(ow)
+    # F itself as a mask gives the grid table
+    x = 980.0 - 20.0 * np.arange(50)
+    a = cheb.ChebTable(50, 1, 1, 3, 3, x, B.CHEB_SHORT_LOWER)
+    b = cheb.ChebTable.from_mask(cheb.cheb_schedule(50, 1, 1, 3), 3, x, B.CHEB_SHORT_LOWER)
+    for s in range(50):
+        assert a.step(s)[1] == b.step(s)[1]
+        assert np.array_equal(a.step(s)[2], b.step(s)[2])
+    # Chebyshev-placed full steps over 50 steps, saved and loaded
+    cheb_steps = np.unique(np.rint(cheb.cheb_chebyshev_nodes(12, 1, 0, 49)).astype(int))
+    mask = np.zeros(50, dtype=bool)
+    mask[cheb_steps] = True
+    t = cheb.ChebTable.from_mask(mask, 4, x, B.CHEB_SHORT_LOWER)
+    path = os.path.join(tmp_path, "cheb_nodes.chebtable")
+    t.save(path)
+    u = cheb.ChebTable.load(path)
+    for s in range(50):
+        assert t.step(s)[1] == u.step(s)[1] and np.array_equal(t.step(s)[2], u.step(s)[2])
