@@ -1,0 +1,106 @@
+"""Edge cases of the device path through the C ABI: non-finite inputs, a
+target on a held node, the largest history the kernels take at the full
+FLUX cache shape, and stream ordering of push and prediction."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_23429_amd as cheb
+from synth import CONFIGS, make_history, split_segments
+from tests.gpu_util import check_parity, say, to_host_bits
+
+pytestmark = pytest.mark.gpu
+
+
+def _classes(v):
+    return np.where(np.isnan(v), 0, np.where(np.isposinf(v), 1, np.where(np.isneginf(v), 2, 3)))
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_nonfinite_inputs_propagate_like_ieee(dtype):
+    """NaN and +-Inf planted in the history: the output is NaN / +-Inf
+    exactly where the fp64 oracle's is, finite elements keep the bound."""
+    td = torch.bfloat16 if dtype == "bf16" else torch.float32
+    n, numel = 5, 100_003
+    g = torch.Generator(device="cuda")
+    g.manual_seed(19)
+    srcs = [torch.randn(numel, generator=g, device="cuda").to(td) for _ in range(n)]
+    rng = np.random.default_rng(19)
+    for k in range(n):
+        for val in (float("nan"), float("inf"), float("-inf")):
+            idx = torch.from_numpy(rng.integers(0, numel, 300)).to("cuda")
+            srcs[k].index_fill_(0, idx, val)
+    w = oracle.weights_row([900, 820, 740, 660, 580], 560)
+    out = torch.empty(numel, dtype=td, device="cuda")
+    cheb.combine(srcs, w, out)
+    torch.cuda.synchronize()
+    hosts = [to_host_bits(s) for s in srcs]
+    exp, mag = (oracle.extrapolate_bf16 if dtype == "bf16" else oracle.extrapolate_f32)(hosts, w)
+    got = oracle.bf16_to_f64(to_host_bits(out)) if dtype == "bf16" else to_host_bits(out).astype(np.float64)
+    fin = np.isfinite(exp)
+    assert (~fin).sum() > 1000
+    assert np.array_equal(_classes(got[~fin]), _classes(exp[~fin]))
+    e = oracle.parity_error(got[fin], exp[fin], mag[fin])[0]
+    assert e <= (1e-2 if dtype == "bf16" else 1e-5)
+
+
+def test_target_on_a_held_node_is_a_bit_copy():
+    cfg = CONFIGS[4].shrunk(400_000)
+    entries = make_history(cfg, "cuda")
+    cache = cheb.ChebCache(cfg.n_hist, torch.bfloat16, cfg.seg_numel)
+    for x, e in zip(cfg.nodes, entries):
+        cache.push(x, split_segments(e, cfg))
+    for j, x in enumerate(cfg.nodes):
+        out, w = cache.extrapolate_at(x)
+        torch.cuda.synchronize()
+        assert w.tolist() == [1.0 if k == j else 0.0 for k in range(cfg.n_hist)]
+        assert torch.equal(out.view(torch.int16), entries[j].view(torch.int16))
+    cache.close()
+
+
+def test_eight_entry_history_full_flux_shape():
+    """K + 1 = 8 (the largest history the kernels take) on the full FLUX
+    cache: eight full steps, sampled against the oracle."""
+    cfg = CONFIGS[4]
+    nodes = [1.0 - s / 50.0 for s in (2, 5, 8, 10, 14, 17, 20, 25)]
+    say(f"eight-entry history: {cfg.numel} elements x 8")
+    entries = make_history(cfg, "cuda", nodes=nodes)
+    cache = cheb.ChebCache(8, torch.bfloat16, cfg.seg_numel)
+    for x, e in zip(nodes, entries):
+        cache.push(x, split_segments(e, cfg))
+    targets = [0.48, 0.44, 0.40]
+    outs, w = cache.extrapolate_at_multi(targets)
+    torch.cuda.synchronize()
+    idx = np.unique(np.random.default_rng(8).integers(0, cfg.numel, 1 << 18))
+    it = torch.from_numpy(idx).to("cuda")
+    hosts = [to_host_bits(e.index_select(0, it)) for e in entries]
+    for m, t in enumerate(targets):
+        check_parity(to_host_bits(outs[m].index_select(0, it)), hosts,
+                     oracle.weights_row(nodes, t), "bf16", f"8 entries t={t}")
+    cache.close()
+    del entries, outs
+    torch.cuda.empty_cache()
+
+
+def test_push_then_predict_ordered_on_one_stream():
+    """Pushes and predictions issued back to back on one non-default stream,
+    with no host synchronisation between them, see each other's writes."""
+    cfg = CONFIGS[1].shrunk(300_000)
+    s = torch.cuda.Stream()
+    entries = make_history(cfg, "cuda", nodes=[900.0, 820.0, 740.0, 660.0, 580.0, 500.0, 420.0])
+    torch.cuda.synchronize()
+    cache = cheb.ChebCache(5, torch.bfloat16, cfg.seg_numel)
+    outs = []
+    with torch.cuda.stream(s):
+        for i, (x, e) in enumerate(zip([900.0, 820.0, 740.0, 660.0, 580.0, 500.0, 420.0], entries)):
+            cache.push(x, split_segments(e, cfg), stream=s)
+            if i >= 4:
+                outs.append((cache.history().tolist(), cache.extrapolate_at(400.0, stream=s)[0]))
+    s.synchronize()
+    hosts = [to_host_bits(e) for e in entries]
+    for hist, out in outs:
+        first = [900.0, 820.0, 740.0, 660.0, 580.0, 500.0, 420.0].index(hist[0])
+        check_parity(to_host_bits(out), hosts[first:first + 5], oracle.weights_row(hist, 400.0),
+                     "bf16", f"history from {hist[0]}")
+    cache.close()
