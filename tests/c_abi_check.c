@@ -17,7 +17,8 @@
     }                                                                      \
   } while (0)
 
-int main(void) {
+int main(int argc, char **argv) {
+  const char *table_path = argc > 1 ? argv[1] : NULL;
   CHECK(cheb_version() == CHEB_VERSION);
   /* Newton one-step-ahead weights for four equispaced nodes: -1 4 -6 4. */
   const double hist[4] = {999.0, 979.0, 959.0, 939.0};
@@ -58,6 +59,52 @@ int main(void) {
   CHECK(cheb_schedule(20, 2, 1, 4, full) == CHEB_OK);
   const int want[20] = {1, 1, 1, 0, 0, 0, 1, 0, 0, 0, 1, 0, 0, 0, 1, 0, 0, 0, 1, 1};
   for (int s = 0; s < 20; ++s) CHECK(full[s] == want[s]);
+
+  /* Offline table: build, query, save, load, compare bit for bit. */
+  double tsteps[50];
+  for (int s = 0; s < 50; ++s) tsteps[s] = 1.0 - s / 50.0;
+  cheb_table *t = NULL, *u = NULL;
+  CHECK(cheb_table_build(&t, 50, 1, 1, 6, 6, tsteps, CHEB_SHORT_LOWER) == CHEB_OK);
+  int32_t T = 0, nh = 0, pol = 0, nfull = 0;
+  CHECK(cheb_table_info(t, &T, &nh, &pol, &nfull) == CHEB_OK && T == 50 && nfull == 10);
+  if (table_path) {
+    CHECK(cheb_table_save(t, table_path) == CHEB_OK);
+    CHECK(cheb_table_load(&u, table_path) == CHEB_OK);
+    for (int s = 0; s < 50; ++s) {
+      int32_t p1, p2, n1, n2, s1[CHEB_MAX_SLOTS], s2[CHEB_MAX_SLOTS];
+      double w1[CHEB_MAX_SLOTS], w2[CHEB_MAX_SLOTS];
+      CHECK(cheb_table_step(t, s, &p1, &n1, s1, w1) == CHEB_OK);
+      CHECK(cheb_table_step(u, s, &p2, &n2, s2, w2) == CHEB_OK);
+      CHECK(p1 == p2 && n1 == n2);
+      CHECK(memcmp(s1, s2, sizeof(int32_t) * (size_t)n1) == 0);
+      CHECK(memcmp(w1, w2, sizeof(double) * (size_t)n1) == 0);
+    }
+    CHECK(cheb_table_destroy(u) == CHEB_OK);
+  }
+  CHECK(cheb_table_load(&u, "/nonexistent/dir/table") == CHEB_E_IO);
+  uint8_t mask[50] = {0};
+  mask[0] = mask[7] = mask[19] = mask[33] = 1;
+  CHECK(cheb_table_build_mask(&u, 50, mask, 3, tsteps, CHEB_SHORT_FULL) == CHEB_OK);
+  CHECK(cheb_table_destroy(u) == CHEB_OK);
+  CHECK(cheb_table_destroy(t) == CHEB_OK);
+
+  /* Refused before any launch: residual and stateless-combination checks. */
+  {
+    const void *src[2] = {fake, (char *)fake + (1 << 20)};
+    double w2[2] = {0.5, 0.5};
+    CHECK(cheb_combine(src, 2, w2, (char *)fake + 8, 100, CHEB_BF16, NULL) == CHEB_E_ALIGN);
+    CHECK(cheb_combine(src, 9, w2, (char *)fake + (2 << 20), 100, CHEB_BF16, NULL) == CHEB_E_INVAL);
+    int64_t segn[2] = {64, 64}, roff[2] = {0, 4};
+    float *xo = (float *)((char *)fake + (4 << 20));
+    CHECK(cheb_residual_reduce(src, segn, roff, 2, CHEB_BF16, NULL, xo, 64, NULL) == CHEB_E_ALIGN);
+    roff[1] = 8;
+    CHECK(cheb_residual_reduce(src, segn, roff, 2, CHEB_BF16, NULL, xo, 64, NULL) == CHEB_E_INVAL);
+    CHECK(cheb_residual_reduce(src, segn, roff, 2, 5, NULL, xo, 64, NULL) == CHEB_E_DTYPE);
+  }
+  double nodes_out[8];
+  CHECK(cheb_chebyshev_nodes(8, 1, 0.0, 49.0, nodes_out) == CHEB_OK && nodes_out[0] > nodes_out[7]);
+  double wv[4];
+  CHECK(cheb_precompute_weights_variant(hist, 4, target, 1, CHEB_RHO_ALTERNATING, wv) == CHEB_OK);
 
   cheb_launch_config cfg;
   CHECK(cheb_get_launch_config(&cfg) == CHEB_OK && cfg.block == 1024);
