@@ -33,8 +33,6 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
-constexpr int kBlock = 256;  // gather kernel: 4 waves of 64 lanes
-
 template <bool NT>
 __device__ __forceinline__ u32x4 load16(const u32x4 *p) {
   if constexpr (NT) return __builtin_nontemporal_load(p);
@@ -288,53 +286,44 @@ hipError_t launch_op(const void *const *src, int n, const double *w, int n_out,
 // ---- full-step push: segment gather into one slot --------------------------
 
 constexpr int kGatherMax = 64;
-constexpr int kGatherUnroll = 4;
-constexpr uint32_t kGatherChunk = kBlock * kGatherUnroll;  // vectors per block
+constexpr int kGatherBlock = 1024;  // one 16-byte vector per lane
+constexpr uint32_t kGatherChunk = kGatherBlock;  // vectors per block
 
 struct GatherArgs {
   const void *src[kGatherMax];
   uint64_t dst_offset[kGatherMax];  // elements
   uint64_t numel[kGatherMax];
-  uint32_t chunk_begin[kGatherMax + 1];  // prefix sums of blocks per segment
   int32_t n;
 };
 
+// Grid: x = 1024-vector chunk within a segment, y = segment.  Blocks past
+// their segment's end return at once, so no block searches for its
+// segment.  Source reads and slot writes are streaming (each byte is touched
+// once per push), so both carry the non-temporal hint.
 template <typename E>
-__global__ __launch_bounds__(kBlock) void gather_kernel(GatherArgs a, char *__restrict__ slot) {
+__global__ __launch_bounds__(kGatherBlock) void gather_kernel(GatherArgs a, char *__restrict__ slot) {
   constexpr int kVec = 16 / int(sizeof(E));
-  // Segment of this block: the last s with chunk_begin[s] <= blockIdx.x.
-  int s = 0;
-  while (s + 1 < a.n && a.chunk_begin[s + 1] <= blockIdx.x) ++s;
-  const uint32_t chunk = blockIdx.x - a.chunk_begin[s];
+  const int s = int(blockIdx.y);
   const uint64_t numel = a.numel[s];
   const uint64_t n_full = numel / kVec;
   const uint32_t rem = uint32_t(numel % kVec);
+  const uint64_t i = uint64_t(blockIdx.x) * kGatherChunk + threadIdx.x;
+  if (i > n_full || (i == n_full && rem == 0)) return;
   const u32x4 *src = static_cast<const u32x4 *>(a.src[s]);
   E *dst_e = reinterpret_cast<E *>(slot) + a.dst_offset[s];
   u32x4 *dst = reinterpret_cast<u32x4 *>(dst_e);
-  const uint64_t base = uint64_t(chunk) * kGatherChunk + threadIdx.x;
-  u32x4 v[kGatherUnroll];
+  if (i < n_full) {
+    store16<true>(dst + i, load16<true>(src + i));
+  } else {
+    // Last, partial vector: copy the remaining elements one by one and zero
+    // the padding up to the 16-byte boundary.
+    const E *src_e = static_cast<const E *>(a.src[s]);
+    E tmp[kVec];
 #pragma unroll
-  for (int u = 0; u < kGatherUnroll; ++u) {
-    const uint64_t i = base + u * kBlock;
-    if (i < n_full) v[u] = src[i];
-  }
-#pragma unroll
-  for (int u = 0; u < kGatherUnroll; ++u) {
-    const uint64_t i = base + u * kBlock;
-    if (i < n_full) {
-      dst[i] = v[u];
-    } else if (i == n_full && rem != 0) {
-      // Last, partial vector: copy the remaining elements one by one and
-      // zero the padding up to the 16-byte boundary.
-      const E *src_e = static_cast<const E *>(a.src[s]);
-      E tmp[kVec];
-#pragma unroll
-      for (int e = 0; e < kVec; ++e) tmp[e] = (uint32_t(e) < rem) ? src_e[n_full * kVec + e] : E(0);
-      u32x4 packed;
-      memcpy(&packed, tmp, 16);
-      dst[i] = packed;
-    }
+    for (int e = 0; e < kVec; ++e) tmp[e] = (uint32_t(e) < rem) ? src_e[n_full * kVec + e] : E(0);
+    u32x4 packed;
+    memcpy(&packed, tmp, 16);
+    dst[i] = packed;
   }
 }
 
@@ -500,7 +489,7 @@ int launch_gather(int dtype, void *slot_base, const GatherSeg *segs, int n_segs,
     const int count = std::min(kGatherMax, n_segs - first);
     GatherArgs a;
     memset(&a, 0, sizeof a);
-    uint32_t blocks = 0;
+    uint64_t max_chunks = 0;
     int used = 0;
     for (int j = 0; j < count; ++j) {
       const GatherSeg &g = segs[first + j];
@@ -510,18 +499,17 @@ int launch_gather(int dtype, void *slot_base, const GatherSeg *segs, int n_segs,
       a.src[used] = g.src;
       a.dst_offset[used] = uint64_t(g.dst_offset);
       a.numel[used] = uint64_t(g.numel);
-      a.chunk_begin[used] = blocks;
-      blocks += uint32_t(chunks);
+      max_chunks = std::max(max_chunks, chunks);
       ++used;
     }
     if (used == 0) continue;
-    a.chunk_begin[used] = blocks;
     a.n = used;
     char *slot = static_cast<char *>(slot_base);
+    const dim3 grid{static_cast<uint32_t>(max_chunks), static_cast<uint32_t>(used), 1u};
     if (dtype == CHEB_BF16)
-      hipLaunchKernelGGL(gather_kernel<uint16_t>, dim3(blocks), dim3(kBlock), 0, stream, a, slot);
+      hipLaunchKernelGGL(gather_kernel<uint16_t>, grid, dim3(kGatherBlock), 0, stream, a, slot);
     else
-      hipLaunchKernelGGL(gather_kernel<float>, dim3(blocks), dim3(kBlock), 0, stream, a, slot);
+      hipLaunchKernelGGL(gather_kernel<float>, grid, dim3(kGatherBlock), 0, stream, a, slot);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return fail(CHEB_E_HIP, "push launch failed: %s", hipGetErrorString(e));
   }
