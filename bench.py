@@ -286,6 +286,29 @@ def cpu_baseline(torch, cfg, entries, targets, seconds, max_host_bytes=16 << 30)
                       f"counts the same algorithmic bytes per element as the GPU step"}
 
 
+def time_graph(torch, cache, targets, out, steps):
+    """Per-step time of `steps` predictions captured once in a HIP graph and
+    replayed (for steps short enough that host launch cost shows)."""
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(g):
+            for i in range(steps):
+                cache.extrapolate_at(targets[i % len(targets)], out)
+    torch.cuda.current_stream().wait_stream(side)
+    g.replay()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(5):
+        g.replay()
+    b.record()
+    b.synchronize()
+    del g
+    return a.elapsed_time(b) / (5 * steps) * 1e3
+
+
 def measure_config(torch, cheb, cfg, steps, warmup):
     entries, cache, push_ms = setup_workload(torch, cheb, cfg)
     out = cache.new_output()
@@ -301,6 +324,10 @@ def measure_config(torch, cheb, cfg, steps, warmup):
         "push_us_median": sorted(push_ms)[len(push_ms) // 2] * 1e3,
         "push_gbps": 2 * cfg.numel * cfg.elem_size / (sorted(push_ms)[len(push_ms) // 2] * 1e6),
     }
+    if region_ms < 0.05:      # launch-bound: also time the steps replayed from a HIP graph
+        g_us = time_graph(torch, cache, cfg.targets, out, 64)
+        res["graph_us_per_step"] = g_us
+        res["graph_gbps"] = B / (g_us * 1e3)
     return res, entries, cache, out
 
 

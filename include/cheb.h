@@ -415,7 +415,8 @@ CHEB_API int cheb_residual_reduce(const void *const *seg_src, const int64_t *seg
  *   blocks_per_cu  0: one block per tile of block x unroll vectors (the grid
  *                covers the whole problem); 1..64: a persistent grid of that
  *                many blocks per compute unit, each looping over tiles.
- * Default {1024, 1, 1, 0}.  Errors: CHEB_E_INVAL. */
+ * Default {1024, 1, 1, 0}; with block 1024, a problem under 4096 vectors
+ * per compute unit runs with 256-thread blocks.  Errors: CHEB_E_INVAL. */
 typedef struct cheb_launch_config {
   int32_t block;
   int32_t unroll;

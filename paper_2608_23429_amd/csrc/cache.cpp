@@ -205,8 +205,9 @@ int cheb_cache_push(cheb_cache *c, double t, const void *const *seg_src, void *s
     }
     segs[s] = GatherSeg{seg_src[s], c->seg_offset[s], c->seg_numel[s]};
   }
-  // The slot receiving the entry is the oldest one when the ring is full.
-  const int32_t slot = (c->count == c->n_slots) ? c->slot_of_age(0) : c->head;
+  // The entry goes to slot `head`: the next free slot, or the oldest entry's
+  // slot when the ring is full.
+  const int32_t slot = c->head;
   rc = launch_gather(c->dtype, c->slot_ptr(slot), segs.data(), int(n_segs),
                      static_cast<hipStream_t>(stream));
   if (rc != CHEB_OK) return rc;

@@ -212,6 +212,10 @@ template <class Op, int NS, bool NT>
 hipError_t launch_one(const Hist<NS, 1, typename Op::W> &h, uint32_t n_vec, Tail tail,
                       const cheb_launch_config &cfg, int cus, hipStream_t s) {
   const int b = cfg.block, u = cfg.unroll, g = cfg.blocks_per_cu;
+  // A problem too small to give every compute unit a few 1024-thread blocks
+  // runs with 256-thread blocks instead (four times as many blocks).
+  const bool small = uint64_t(n_vec) < uint64_t(4 * 1024) * uint64_t(cus);
+  if (b == 1024 && small) return launch_shape<Op, NS, 1, 256, 1, NT>(h, n_vec, tail, g, cus, s);
   if (b == 1024) return launch_shape<Op, NS, 1, 1024, 1, NT>(h, n_vec, tail, g, cus, s);
   if (b == 512) {
     if (u == 1) return launch_shape<Op, NS, 1, 512, 1, NT>(h, n_vec, tail, g, cus, s);

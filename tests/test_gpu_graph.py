@@ -1,0 +1,50 @@
+"""Skipped-step predictions captured in a HIP graph (torch.cuda.CUDAGraph)
+and replayed: the library only launches kernels (no allocation, no memset),
+so captured predictions replay to the same bits as eager ones.  Every
+replay is checked, with eager work and synchronisation in between.  Pushes
+are not captured: they update host-side ring state at call time."""
+import numpy as np
+import pytest
+import torch
+
+import paper_2608_23429_amd as cheb
+from synth import CONFIGS, make_history, split_segments
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("cfg", [CONFIGS[0], CONFIGS[4].shrunk(2_000_000)], ids=["tiny", "flux_small"])
+def test_predictions_replay_from_a_graph(cfg):
+    dt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    entries = make_history(cfg, "cuda")
+    cache = cheb.ChebCache(cfg.n_hist, dt, cfg.seg_numel)
+    for x, e in zip(cfg.nodes, entries):
+        cache.push(x, split_segments(e, cfg))
+    torch.cuda.synchronize()
+    eager = [cache.extrapolate_at(t)[0].clone() for t in cfg.targets]
+    eager_multi = cache.extrapolate_at_multi(cfg.targets)[0]
+    torch.cuda.synchronize()
+    outs = [cache.new_output() for _ in cfg.targets]
+    outs_multi = [cache.new_output() for _ in cfg.targets]
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(g):
+            for t, o in zip(cfg.targets, outs):
+                cache.extrapolate_at(t, o)
+            cache.extrapolate_at_multi(cfg.targets, outs_multi)
+    torch.cuda.current_stream().wait_stream(side)
+    view = torch.int16 if dt == torch.bfloat16 else torch.int32
+    for rep in range(4):
+        for o in outs + outs_multi:
+            o.zero_()                               # eager work between replays
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for o, e in zip(outs, eager):
+            assert torch.equal(o.view(view), e.view(view)), rep
+        for o, e in zip(outs_multi, eager_multi):
+            assert torch.equal(o.view(view), e.view(view)), rep
+    del g
+    cache.close()
