@@ -2,13 +2,13 @@
 //
 // 1. The skipped-step prediction (paper, Section 3.3, forward application
 //    equation; Algorithm 1, extrapolation branch): out = sum_k w_k H_k over
-//    the flattened feature cache, for one target or for several targets
-//    at once (all of them depend on the same history).  Pure streaming work: (n+1) x 16 bytes of
-//    HBM traffic per 16-byte output vector and 2n flops per element, far
-//    below the fp32 ridge point, so the kernel is laid out for bandwidth:
-//    128-bit coalesced loads (a wave covers 1 KiB contiguous per load
-//    instruction), all n x unroll loads of a thread issued before any
-//    arithmetic, weights as kernel arguments (they live in SGPRs), fp32
+//    the flattened feature cache, for one target or for several targets at
+//    once (all of them depend on the same history).  Pure streaming work:
+//    (n+1) x 16 bytes of HBM traffic per 16-byte output vector and 2n flops
+//    per element, far below the fp32 ridge point, so the kernel is laid out
+//    for bandwidth: 128-bit coalesced loads (a wave covers 1 KiB contiguous
+//    per load instruction), all n x unroll loads of a thread issued before
+//    any arithmetic, weights as kernel arguments (they live in SGPRs), fp32
 //    accumulation for bf16 storage and fp64 for fp32 storage, and one
 //    hardware round-to-nearest-even pack per element pair
 //    (v_cvt_pk_bf16_f32).  No LDS: nothing is reused across lanes.
