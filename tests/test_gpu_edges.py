@@ -104,3 +104,51 @@ def test_push_then_predict_ordered_on_one_stream():
         check_parity(to_host_bits(out), hosts[first:first + 5], oracle.weights_row(hist, 400.0),
                      "bf16", f"history from {hist[0]}")
     cache.close()
+
+
+def _max_numel(dtype):
+    """Largest element count one launch takes: 2^31 - 1 whole 16-byte
+    vectors plus a ragged tail of one element less than a vector."""
+    per_vec = 8 if dtype == "bf16" else 4
+    return ((1 << 31) - 1) * per_vec + per_vec - 1
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_largest_launch(dtype):
+    """The largest problem the host accepts in one launch (32 GiB per
+    buffer; the kernel's 32-bit vector indices reach 2^31 - 1): two sources,
+    then two outputs from one pass, sampled against the oracle at both ends,
+    around the last tile and at random."""
+    numel = _max_numel(dtype)
+    nbytes = numel * (2 if dtype == "bf16" else 4)
+    free, _ = torch.cuda.mem_get_info()
+    if free < 4 * nbytes + (8 << 30):
+        pytest.skip(f"needs {4 * nbytes + (8 << 30)} free bytes, {free} free")
+    say(f"largest launch {dtype}: {numel} elements, {nbytes} bytes per buffer")
+    td = torch.bfloat16 if dtype == "bf16" else torch.float32
+    g = torch.Generator(device="cuda")
+    g.manual_seed(31)
+    srcs = [torch.empty(numel, dtype=td, device="cuda").uniform_(-1.0, 1.0, generator=g)
+            for _ in range(2)]
+    outs = [torch.empty(numel, dtype=td, device="cuda") for _ in range(2)]
+    nodes, targets = [0.0, 1.0], [1.25, 2.0]
+    w = cheb.precompute_weights(nodes, targets)
+    cheb.combine(srcs, w[0], outs[0])
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(31)
+    idx = np.unique(np.concatenate([
+        np.arange(4096), np.arange(numel - 16384, numel),
+        np.arange((numel // 2) - 2048, (numel // 2) + 2048),
+        rng.integers(0, numel, 1 << 20)]))
+    it = torch.from_numpy(idx).to("cuda")
+    hosts = [to_host_bits(s.index_select(0, it)) for s in srcs]
+    check_parity(to_host_bits(outs[0].index_select(0, it)), hosts,
+                 oracle.weights_row(nodes, targets[0]), dtype, f"largest single {dtype}")
+    outs[0].zero_()
+    cheb.combine_multi(srcs, w, outs)
+    torch.cuda.synchronize()
+    for m, t in enumerate(targets):
+        check_parity(to_host_bits(outs[m].index_select(0, it)), hosts,
+                     oracle.weights_row(nodes, t), dtype, f"largest multi {dtype} t={t}")
+    del srcs, outs
+    torch.cuda.empty_cache()
