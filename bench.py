@@ -177,7 +177,9 @@ def time_residual(torch, cheb, cfg, entries, cache, steps, warmup):
     output added into the residual stream): the full form over the whole
     history (cheb_residual_apply), and the collapsed history (push-time
     reduction per full step, cheb_residual_reduce, then the prediction from
-    residual-sized entries)."""
+    residual-sized entries; the entry either reduced from the module outputs
+    or taken as the difference of the residual stream across the block
+    stack)."""
     from synth import split_segments
     res_off, res_n = cfg.residual_map()
     stream = torch.cuda.current_stream()
@@ -212,6 +214,15 @@ def time_residual(torch, cheb, cfg, entries, cache, steps, warmup):
                   stream=stream)
         k[0] += 1
     us_reduce = timed(push_one, max(5, steps // 5))
+    x_after = torch.randn(res_n, device="cuda")
+
+    def push_diff():
+        hist.push_difference(cfg.nodes[k[0] % cfg.n_hist] + 1e-3 * (1 + k[0]), x_after, x_in,
+                             stream=stream)
+        k[0] += 1
+    us_diff = timed(push_diff, max(5, steps // 5))
+    for x, sg in zip(cfg.nodes, segs):
+        hist.push(x, sg, stream=stream)
     wc = cheb.cheb_precompute_weights(hist.history(), [float(hist.history()[-1]) - 0.02])[0]
     us_pred = timed(lambda: hist.cache.residual_apply(wc, [0], x_out, x_in, stream=stream), steps)
     hist.close()
@@ -219,6 +230,10 @@ def time_residual(torch, cheb, cfg, entries, cache, steps, warmup):
         "full_form": {"us": us_full, "bytes": cfg.n_hist * S + 2 * R,
                       "gbps": (cfg.n_hist * S + 2 * R) / (us_full * 1e3)},
         "collapsed_push_reduce": {"us": us_reduce, "bytes": S + R, "gbps": (S + R) / (us_reduce * 1e3)},
+        "collapsed_push_difference": {"us": us_diff, "bytes": 3 * R,
+                                      "gbps": 3 * R / (us_diff * 1e3),
+                                      "note": "entry as x_after - x_before of the full step's "
+                                              "residual stream"},
         "collapsed_predict": {"us": us_pred, "bytes": (cfg.n_hist + 2) * R,
                               "gbps": (cfg.n_hist + 2) * R / (us_pred * 1e3)},
         "residual_elements": res_n,
@@ -419,7 +434,8 @@ def main(argv=None):
     resid = time_residual(torch, cheb, cfg, entries, cache, max(10, args.steps // 2), args.warmup)
     log(f"[bench] {cfg.name} residual: full form {resid['full_form']['us']:.1f} us, collapsed "
         f"predict {resid['collapsed_predict']['us']:.1f} us + push-time reduce "
-        f"{resid['collapsed_push_reduce']['us']:.1f} us per full step")
+        f"{resid['collapsed_push_reduce']['us']:.1f} us (or residual difference "
+        f"{resid['collapsed_push_difference']['us']:.1f} us) per full step")
     par = parity_sample(torch, cfg, entries, cache, out, cfg.targets[-1])
     log(f"[bench] parity sample: floored error {par['floored_rel_err']:.3e}")
     achieved = res["bytes_per_step"] / (res["launch_us_avg"] * 1e3)

@@ -186,6 +186,26 @@ class ResidualHistory:
             raise
         self.cache.commit(t)
 
+    def push_difference(self, t: float, x_after: torch.Tensor, x_before: torch.Tensor,
+                        stream: Optional[torch.cuda.Stream] = None):
+        """Entry taken from the residual stream itself.  A full step's block
+        stack leaves x_after = x_before + (every module output added into
+        the residual), so the entry is x_after - x_before: one launch of
+        the combination kernel with weights (1, -1) over residual-sized fp32
+        tensors, instead of a pass over every module output.  The difference
+        is formed in fp64 and rounded once to fp32."""
+        for name, x in (("x_after", x_after), ("x_before", x_before)):
+            if x.dtype != torch.float32 or x.numel() != self.res_numel:
+                raise ChebError(_binding.CHEB_E_MISMATCH,
+                                f"{name} must be float32 with {self.res_numel} elements")
+        slot = self.cache.begin_push()
+        try:
+            combine([x_after, x_before], [1.0, -1.0], slot[:self.res_numel], stream=stream)
+        except Exception:
+            self.cache.reset()
+            raise
+        self.cache.commit(t)
+
     def history(self):
         return self.cache.history()
 

@@ -141,6 +141,59 @@ def test_collapsed_history_equals_full_form(case):
     hist.close()
 
 
+# Entries rounded once to fp32 from an exact fp64 difference: per element the
+# error is at most 2^-24 * sum_k |w_k| |d_k| (entries) plus 2^-24 |o| (the
+# output), so the floored error stays below (1 + 10^3) * 2^-24 = 6.0e-5.
+DIFF_TOL = 1e-4
+
+
+@pytest.mark.parametrize("case", SMALL[:3], ids=lambda c: c[0])
+def test_collapsed_history_from_residual_difference(case):
+    """The collapsed entry taken as x_after - x_before of a full step's
+    block stack (ResidualHistory.push_difference), against the oracle's
+    x_in + sum_k w_k (x_after_k - x_before_k) in fp64; and, by the block
+    equation, the same entries as the push-time reduction of the module
+    outputs up to the fp32 rounding of x_after."""
+    cfg = case[1]()
+    res_off, res_n = cfg.residual_map()
+    entries = make_history(cfg, "cuda")
+    lay = cheb.cheb_cache_layout(1, cheb.CHEB_BF16, cfg.seg_numel)
+    seg_off = [int(o) for o in lay["seg_offset"]]
+    befores, afters = [], []
+    for k, e in enumerate(entries):
+        xb = _x_in(res_n, 100 + k)
+        full, _ = oracle.residual([to_host_bits(e)], [1.0], seg_off, cfg.seg_numel, res_off, res_n,
+                                  x_in=xb.cpu().numpy())
+        befores.append(xb)
+        afters.append(torch.from_numpy(full.astype(np.float32)).to("cuda"))
+    diff = cheb.ResidualHistory(cfg.n_hist, res_off, res_n)
+    red = cheb.ResidualHistory(cfg.n_hist, res_off, res_n)
+    for x, e, xa, xb in zip(cfg.nodes, entries, afters, befores):
+        diff.push_difference(x, xa, xb)
+        red.push(x, split_segments(e, cfg))
+    torch.cuda.synchronize()
+    for k in range(cfg.n_hist):
+        d = diff.cache.entry(k)[:res_n].double()
+        r = red.cache.entry(k)[:res_n].double()
+        scale = (afters[k].double().abs() + befores[k].double().abs()).max().item()
+        assert (d - r).abs().max().item() <= 4 * 2.0 ** -24 * scale, k
+    hosts_a = [a.cpu().numpy() for a in afters]
+    hosts_b = [b.cpu().numpy() for b in befores]
+    x_in = _x_in(res_n, 12)
+    for t in cfg.targets:
+        x_out = torch.empty_like(x_in)
+        _, w = diff.predict(t, x_out, x_in)
+        torch.cuda.synchronize()
+        w_or = oracle.weights_row(cfg.nodes, t)
+        exp, mag = oracle.residual(hosts_a + hosts_b, np.concatenate([w_or, -w_or]), [0], [res_n],
+                                   [0], res_n, x_in=x_in.cpu().numpy(), dtype="f32")
+        _check(x_out.cpu().numpy(), exp, mag, DIFF_TOL, f"difference-form t={t}")
+    with pytest.raises(cheb.ChebError):
+        diff.push_difference(0.0, afters[0][:-4], befores[0][:-4])
+    diff.close()
+    red.close()
+
+
 def _compact_problem(cfg, entries, res_off, res_n, seg_off, idx):
     """Sampled residual elements idx: per segment, the source value each
     sampled element receives (zero where the segment does not cover it), so
