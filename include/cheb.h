@@ -62,13 +62,14 @@ extern "C" {
 typedef enum cheb_status {
   CHEB_OK = 0,
   CHEB_E_INVAL = -1,     /* null pointer, count or enum out of range */
-  CHEB_E_DUPNODE = -2,   /* two equal history abscissae */
+  CHEB_E_DUPNODE = -2,   /* two equal history abscissae (also once mapped onto [-1, 1]) */
   CHEB_E_NOTREADY = -3,  /* history holds fewer than n entries, or a push is open */
   CHEB_E_DTYPE = -4,     /* unknown storage type */
   CHEB_E_ALIGN = -5,     /* device pointer not aligned as documented */
   CHEB_E_HIP = -6,       /* the HIP runtime reported an error */
   CHEB_E_MISMATCH = -7,  /* sizes disagree (arena too small, ...) */
-  CHEB_E_NONFINITE = -8, /* NaN or infinite abscissa or weight */
+  CHEB_E_NONFINITE = -8, /* NaN or infinite abscissa or weight, or a weight row
+                            past fp64's resolution (see cheb_precompute_weights) */
   CHEB_E_IO = -9         /* table file cannot be read or written, or is malformed */
 } cheb_status;
 
@@ -96,6 +97,14 @@ CHEB_API int cheb_version(void);
  *            history abscissa gets the unit row of that entry.
  *   w_out    [n_target][n_hist] host fp64, row-major, caller-owned.  Row m
  *            sums to 1 up to rounding.
+ *
+ * The products of the second form are carried with a separate power-of-two
+ * exponent, so closely clustered abscissae do not underflow them.  A row is
+ * refused (CHEB_E_NONFINITE) when a weight is not finite or when
+ * n_hist * 2^-53 * sum_j |w_j|, the second form's bound on each weight's
+ * relative rounding error, exceeds 2^-24: fp64 then no longer gives the
+ * coefficients to the fp32 precision the bf16 kernel uses them at.  Distinct
+ * abscissae that the map onto [-1, 1] rounds together are CHEB_E_DUPNODE.
  *
  * 1 <= n_hist <= CHEB_MAX_NODES, n_target >= 0.  Errors: CHEB_E_INVAL,
  * CHEB_E_NONFINITE, CHEB_E_DUPNODE.  w_out is not written on error. */

@@ -1,5 +1,6 @@
 // Host side of libcheb: error reporting, launch shape, weight
 // precomputation and the stateless combination entry point.
+#include <limits.h>
 #include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
@@ -65,6 +66,25 @@ int device_cus(int *cus) {
   return CHEB_OK;
 }
 
+// A computed row is refused when a weight is not finite, or when the
+// rounding error of the second form, bounded by about n 2^-53 sum_j |w_j|
+// relative to each weight, could exceed the fp32 resolution (2^-24) at which
+// the bf16 kernel consumes the row: past that point fp64 no longer delivers
+// the coefficients to the precision they are used at.
+static int check_row(const double *w, int n, double target) {
+  double mass = 0.0;
+  for (int j = 0; j < n; ++j) {
+    if (!isfinite(w[j]))
+      return fail(CHEB_E_NONFINITE, "weight %d is not finite (target %.17g)", j, target);
+    mass += fabs(w[j]);
+  }
+  if (double(n) * mass * 0x1p-53 > 0x1p-24)
+    return fail(CHEB_E_NONFINITE,
+                "weights too ill-conditioned for fp64 (sum |w| = %.3g, target %.17g)", mass,
+                target);
+  return CHEB_OK;
+}
+
 // Barycentric coefficients of one target (Section 3.2, coefficient
 // equation; Appendix A, rho_j = 1 / omega'(x_j) and the second form).
 // The abscissae are first mapped affinely so their span becomes [-1, 1]
@@ -100,22 +120,49 @@ int weights_row(const double *x, int n, double target, double *w) {
   double y[CHEB_MAX_NODES];
   for (int j = 0; j < n; ++j) y[j] = (x[j] - mid) * inv_half;
   const double yt = (target - mid) * inv_half;
-  double terms[CHEB_MAX_NODES];
-  double total = 0.0;
+  // term_j = 1 / (omega'(y_j) (yt - y_j)).  The product is carried as a
+  // mantissa in [0.5, 1) and a power of two, so nodes clustered closely
+  // enough for omega' to leave the double range still give their weights:
+  // the second form is unchanged by a common factor, and every term is
+  // scaled by the same power of two before the sum.  Where nothing leaves
+  // the range the result is bit for bit that of the plain product.
+  double inv[CHEB_MAX_NODES];
+  long expo[CHEB_MAX_NODES];
+  long top = LONG_MIN;
   for (int j = 0; j < n; ++j) {
-    double omega_prime = 1.0;
-    for (int k = 0; k < n; ++k)
-      if (k != j) omega_prime *= y[j] - y[k];
     const double gap = yt - y[j];
     if (gap == 0.0) {  // distinct abscissae that the map rounded together
       for (int k = 0; k < n; ++k) w[k] = (k == j) ? 1.0 : 0.0;
       return CHEB_OK;
     }
-    terms[j] = 1.0 / (omega_prime * gap);
+    double m = 1.0;
+    long e = 0;
+    for (int k = 0; k < n; ++k) {
+      if (k == j) continue;
+      const double d = y[j] - y[k];
+      if (d == 0.0)
+        return fail(CHEB_E_DUPNODE,
+                    "history abscissae %d and %d coincide once mapped onto [-1, 1]", k, j);
+      int ex = 0;
+      m = frexp(m * d, &ex);
+      e += ex;
+    }
+    int ex = 0;
+    m = frexp(m * gap, &ex);
+    e += ex;
+    inv[j] = 1.0 / m;  // magnitude in (1, 2]
+    expo[j] = -e;
+    top = expo[j] > top ? expo[j] : top;
+  }
+  double terms[CHEB_MAX_NODES];
+  double total = 0.0;
+  for (int j = 0; j < n; ++j) {
+    const long shift = expo[j] - top;  // <= 0
+    terms[j] = ldexp(inv[j], shift < -2000 ? -2000 : int(shift));
     total += terms[j];
   }
   for (int j = 0; j < n; ++j) w[j] = terms[j] / total;
-  return CHEB_OK;
+  return check_row(w, n, target);
 }
 
 // Coefficients from the alternating weights printed in Section 3.2,
@@ -146,7 +193,7 @@ int weights_row_alternating(const double *x, int n, double target, double *w) {
     total += w[j];
   }
   for (int j = 0; j < n; ++j) w[j] /= total;
-  return CHEB_OK;
+  return check_row(w, n, target);
 }
 
 }  // namespace cheb

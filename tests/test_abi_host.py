@@ -109,6 +109,62 @@ def test_weights_errors_leave_output_untouched():
     assert cheb.cheb_precompute_weights(np.arange(64.0), []).shape == (0, 64)
 
 
+def _clustered(count=30, step=2.0 ** -40):
+    """Two end nodes at -1 and 1 (the map onto [-1, 1] is then the identity)
+    and `count` nodes `step` apart at 0: omega'(x_j) of a clustered node is
+    about step^(count-1), below the smallest double for these defaults."""
+    return [-1.0] + [k * step for k in range(count)] + [1.0]
+
+
+def test_weights_of_clustered_nodes_match_exact():
+    """The products of the second form leave the double range here; the
+    weights still match the exact rational Lagrange coefficients (Appendix
+    A, Lagrange basis) at targets inside the cluster, each to within the
+    second form's rounding bound n 2^-53 sum|w| relative to itself."""
+    from tests.lagrange_exact import lagrange_weights
+    x = _clustered()
+    assert abs(math.prod(x[1] - v for v in x[2:])) < 1e-300
+    for target in [14.5 * 2.0 ** -40, 3.25 * 2.0 ** -40, 27.75 * 2.0 ** -40]:
+        w = cheb.cheb_precompute_weights(x, [target])[0]
+        exact = np.array([float(v) for v in lagrange_weights(x, target)])
+        mass = float(np.abs(exact).sum())
+        bound = 4 * len(x) * 2.0 ** -53 * mass
+        assert np.all(np.abs(w - exact) <= bound * np.abs(exact) + 1e-300), (target, mass)
+
+
+def test_weights_beyond_fp64_resolution_are_an_error():
+    """Where the second form's rounding bound n 2^-53 sum|w| passes 2^-24
+    (the fp32 resolution the bf16 kernel uses the row at), or the exact
+    coefficients exceed the double range, the call fails with
+    CHEB_E_NONFINITE and leaves w_out alone."""
+    from tests.lagrange_exact import lagrange_weights
+    x = _clustered()
+    t_ill = 29.5 * 2.0 ** -40
+    mass = float(sum(abs(v) for v in lagrange_weights(x, t_ill)))
+    assert len(x) * 2.0 ** -53 * mass > 2.0 ** -24
+    assert max(abs(v) for v in lagrange_weights(x, 0.5)) > 2 ** 1024
+    h = np.array(x)
+    for target in (t_ill, 0.5):
+        t = np.array([target])
+        w = np.full((1, len(x)), 7.0)
+        rc = B.LIB.cheb_precompute_weights(B._dptr(h), len(x), B._dptr(t), 1, B._dptr(w))
+        assert rc == B.CHEB_E_NONFINITE, target
+        assert np.all(w == 7.0)
+        assert "not finite" in cheb.cheb_last_error() or "ill-conditioned" in cheb.cheb_last_error()
+
+
+def test_nodes_that_the_map_merges_are_duplicates():
+    """Distinct abscissae that round to one value once mapped onto [-1, 1]
+    are reported as duplicates instead of giving non-finite weights."""
+    x = [-7.002881094626153, -6.668508865894732, -6.668508865894731, 4.804184990778926]
+    mid, inv_half = 0.5 * (x[0] + x[3]), 2.0 / (x[3] - x[0])
+    assert x[1] != x[2] and (x[1] - mid) * inv_half == (x[2] - mid) * inv_half
+    with pytest.raises(cheb.ChebError) as e:
+        cheb.cheb_precompute_weights(x, [5.0])
+    assert e.value.code == B.CHEB_E_DUPNODE
+    assert "coincide" in str(e.value) or "coincide" in cheb.cheb_last_error()
+
+
 # --------------------------------------------------------------------------
 # Layout
 # --------------------------------------------------------------------------

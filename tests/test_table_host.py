@@ -19,6 +19,13 @@ def _wtol(w, factor=16.0):
     return factor * max(1, len(w)) * 2.0 ** -53 * s * max(s, 1.0)
 
 
+def _sampler_grid(rng, T, top=1000.0):
+    """Decreasing timesteps whose spacing varies by at most 3x, as in a
+    sampler's schedule (the rows stay well inside fp64's resolution)."""
+    gaps = rng.uniform(0.5, 1.5, size=T) * (top / max(T, 1))
+    return (top - np.concatenate([[0.0], np.cumsum(gaps[:-1])]))
+
+
 def test_schedule_matches_golden_and_oracle():
     with open(os.path.join(GOLDEN, "full_schedule.txt")) as f:
         for line in f:
@@ -60,7 +67,7 @@ def test_table_matches_oracle_simulation(policy):
         T = int(rng.integers(2, 60))
         s0, s1, r = int(rng.integers(0, 5)), int(rng.integers(0, 5)), int(rng.integers(1, 8))
         n = int(rng.integers(1, 9))
-        x = np.sort(rng.uniform(0, 1000, size=T))[::-1].copy()   # decreasing timesteps
+        x = _sampler_grid(rng, T)
         _compare_table(T, s0, s1, r, n, x, policy)
 
 
@@ -139,6 +146,19 @@ def test_table_errors():
     assert e.value.code == B.CHEB_E_INVAL
 
 
+def test_table_with_an_ill_conditioned_row_is_refused():
+    """Three full steps a thousandth apart predicting a step 500 away: the
+    row's sum |w| (about 2.5e11) is past what fp64 resolves to fp32
+    accuracy, so the build fails instead of storing it."""
+    x = np.array([1000.0, 999.999, 999.998, 500.0, 400.0])
+    mask = np.array([True, True, True, False, True])
+    kind, _, ow = oracle.table_row_mask(mask, 3, x, B.CHEB_SHORT_FULL, 3)
+    assert kind == 1 and 3 * 2.0 ** -53 * np.abs(ow).sum() > 2.0 ** -24
+    with pytest.raises(cheb.ChebError) as e:
+        cheb.ChebTable.from_mask(mask, 3, x, B.CHEB_SHORT_FULL)
+    assert e.value.code == B.CHEB_E_NONFINITE
+
+
 def test_extrapolate_steps_checks_ring_against_row():
     """Row selection (the history must hold the row's nodes) is checked on
     the host before anything is enqueued."""
@@ -177,7 +197,7 @@ def test_mask_tables_match_oracle_and_roundtrip(tmp_path):
             T = int(rng.integers(2, 50))
             mask = rng.random(T) < rng.uniform(0.1, 0.6)
             n = int(rng.integers(1, 7))
-            x = np.sort(rng.uniform(0, 1, T))[::-1].copy()
+            x = _sampler_grid(rng, T, 1.0)
             t = cheb.ChebTable.from_mask(mask, n, x, policy)
             for s in range(T):
                 pred, nodes, w = t.step(s)
