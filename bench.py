@@ -490,6 +490,22 @@ def main(argv=None):
             del e, ch, o
             torch.cuda.empty_cache()
         line["per_config"] = per
+        shares = []
+        for g in (2, 4, 8):
+            c = cfg.scaled_blocks(g, 1 << 30)
+            r, e, ch, o = measure_config(torch, cheb, c, max(10, args.steps // 2), args.warmup)
+            log(f"[bench] {cfg.name} 1/{g} token share: {r['us_per_step']:.1f} us/step, "
+                f"{r['gbps']:.0f} GB/s")
+            shares.append({"share": f"1/{g}", "elements": r["elements"],
+                           "bytes_per_step": r["bytes_per_step"], "us_per_step": r["us_per_step"],
+                           "gbps": r["gbps"], "launch_us_median": r["launch_us_median"]})
+            ch.close()
+            del e, ch, o
+            torch.cuda.empty_cache()
+        line["token_shares"] = {
+            "workload": cfg.name, "shares": shares,
+            "note": "one GPU's part of the cache when the model is split G ways along the token "
+                    "axis (every cached tensor's token dimension divided by G); not in value"}
     print(json.dumps(line), flush=True)
     return 0
 
