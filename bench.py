@@ -243,7 +243,9 @@ def time_residual(torch, cheb, cfg, entries, cache, steps, warmup):
     }
 
 
-def parity_sample(torch, cfg, entries, cache, out, target, count=1 << 16):
+def oracle_parity_sample(torch, cfg, entries, cache, out, target, count=1 << 16):
+    """Part of the CPU-baseline leg: the same oracle, untimed, recomputes a
+    sample of the device's prediction at `target` from the stored history."""
     import numpy as np
     import oracle
     idx = np.unique(np.random.default_rng(cfg.seed).integers(0, cfg.numel, count))
@@ -436,8 +438,6 @@ def main(argv=None):
         f"predict {resid['collapsed_predict']['us']:.1f} us + push-time reduce "
         f"{resid['collapsed_push_reduce']['us']:.1f} us (or residual difference "
         f"{resid['collapsed_push_difference']['us']:.1f} us) per full step")
-    par = parity_sample(torch, cfg, entries, cache, out, cfg.targets[-1])
-    log(f"[bench] parity sample: floored error {par['floored_rel_err']:.3e}")
     achieved = res["bytes_per_step"] / (res["launch_us_avg"] * 1e3)
     traffic = measured_traffic(cfg.name)
     line = {
@@ -467,13 +467,15 @@ def main(argv=None):
                  "note": "full-step copy into the ring, once per full step (not in value)"},
         "multi_target": multi,
         "residual": resid,
-        "parity_sample": par,
     }
     if not args.no_cpu_baseline:
         log(f"[bench] oracle CPU baseline (~{args.cpu_seconds:.0f} s)")
         line["cpu_baseline"] = cpu_baseline(torch, cfg, entries, cfg.targets, args.cpu_seconds)
         log(f"[bench] oracle: {line['cpu_baseline']['value']:.2f} GB/s on "
             f"{line['cpu_baseline']['cores']} threads")
+        par = oracle_parity_sample(torch, cfg, entries, cache, out, cfg.targets[-1])
+        line["cpu_baseline"]["parity_sample"] = par
+        log(f"[bench] oracle parity sample: floored error {par['floored_rel_err']:.3e}")
     cache.close()
     del entries, cache, out
     torch.cuda.empty_cache()
