@@ -403,7 +403,7 @@ def main(argv=None):
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU only: the skipped-step prediction needs no "
-              "communication, and this build runs on a single MI355X. Run with --gpus 1.",
+              "communication, and this benchmark runs on a single MI355X. Run with --gpus 1.",
               file=sys.stderr, flush=True)
         return 2
     import torch

@@ -7,7 +7,7 @@ import torch
 
 import oracle
 import paper_2608_23429_amd as cheb
-from synth import CONFIGS, make_history, split_segments
+from synth import CONFIGS, make_history, split_segments, by_name
 from tests.gpu_util import check_parity, say, to_host_bits
 
 pytestmark = pytest.mark.gpu
@@ -46,7 +46,7 @@ def test_nonfinite_inputs_propagate_like_ieee(dtype):
 
 
 def test_target_on_a_held_node_is_a_bit_copy():
-    cfg = CONFIGS[4].shrunk(400_000)
+    cfg = by_name("flux_dev_1024").shrunk(400_000)
     entries = make_history(cfg, "cuda")
     cache = cheb.ChebCache(cfg.n_hist, torch.bfloat16, cfg.seg_numel)
     for x, e in zip(cfg.nodes, entries):
@@ -62,7 +62,7 @@ def test_target_on_a_held_node_is_a_bit_copy():
 def test_eight_entry_history_full_flux_shape():
     """K + 1 = 8 (the largest history the kernels take) on the full FLUX
     cache: eight full steps, sampled against the oracle."""
-    cfg = CONFIGS[4]
+    cfg = by_name("flux_dev_1024")
     nodes = [1.0 - s / 50.0 for s in (2, 5, 8, 10, 14, 17, 20, 25)]
     say(f"eight-entry history: {cfg.numel} elements x 8")
     entries = make_history(cfg, "cuda", nodes=nodes)
@@ -86,7 +86,7 @@ def test_eight_entry_history_full_flux_shape():
 def test_push_then_predict_ordered_on_one_stream():
     """Pushes and predictions issued back to back on one non-default stream,
     with no host synchronisation between them, see each other's writes."""
-    cfg = CONFIGS[1].shrunk(300_000)
+    cfg = by_name("dit_xl2_256").shrunk(300_000)
     s = torch.cuda.Stream()
     entries = make_history(cfg, "cuda", nodes=[900.0, 820.0, 740.0, 660.0, 580.0, 500.0, 420.0])
     torch.cuda.synchronize()

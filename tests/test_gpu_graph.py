@@ -8,12 +8,12 @@ import pytest
 import torch
 
 import paper_2608_23429_amd as cheb
-from synth import CONFIGS, make_history, split_segments
+from synth import CONFIGS, make_history, split_segments, by_name
 
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("cfg", [CONFIGS[0], CONFIGS[4].shrunk(2_000_000)], ids=["tiny", "flux_small"])
+@pytest.mark.parametrize("cfg", [by_name("tiny"), by_name("flux_dev_1024").shrunk(2_000_000)], ids=["tiny", "flux_small"])
 def test_predictions_replay_from_a_graph(cfg):
     dt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
     entries = make_history(cfg, "cuda")

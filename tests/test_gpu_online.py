@@ -9,7 +9,7 @@ import torch
 
 import oracle
 import paper_2608_23429_amd as cheb
-from synth import CONFIGS, make_history, split_segments
+from synth import CONFIGS, make_history, split_segments, by_name
 from tests.gpu_util import check_parity, say, to_host_bits
 
 pytestmark = pytest.mark.gpu
@@ -65,7 +65,7 @@ def test_online_stage(case):
 
 def test_table_row_must_match_ring():
     """A table built for another abscissa grid is refused before launch."""
-    cfg = CONFIGS[4].shrunk(50_000)
+    cfg = by_name("flux_dev_1024").shrunk(50_000)
     x = 1.0 - np.arange(20) / 20.0
     table = cheb.ChebTable(20, 1, 1, 4, 2, x)
     cache = cheb.ChebCache(2, torch.bfloat16, cfg.seg_numel)

@@ -11,7 +11,7 @@ import torch
 
 import oracle
 import paper_2608_23429_amd as cheb
-from synth import CONFIGS, make_history, split_segments
+from synth import CONFIGS, make_history, split_segments, by_name
 from tests.gpu_util import TOL, check_parity, decode, say, to_host_bits
 
 pytestmark = pytest.mark.gpu
@@ -285,7 +285,7 @@ def test_tiny_recovers_quadratic():
     The prediction at the next timesteps equals the quadratic at the target
     up to the combined noise (|w| sums to at most 2.14 here) and fp32
     storage rounding."""
-    cfg = CONFIGS[0]
+    cfg = by_name("tiny")
     cache, entries, outs, ws = _run_workload(cfg, cfg.nodes, cfg.targets)
     g = torch.Generator(device="cuda")
     g.manual_seed(cfg.seed)

@@ -7,7 +7,7 @@ import torch
 
 import oracle
 import paper_2608_23429_amd as cheb
-from synth import CONFIGS, make_history, split_segments
+from synth import CONFIGS, make_history, split_segments, by_name
 from tests.gpu_util import say, to_host_bits
 
 pytestmark = pytest.mark.gpu
@@ -39,10 +39,10 @@ def _x_in(n, seed):
 
 
 SMALL = [
-    ("dit", lambda: CONFIGS[1].scaled_blocks(16, 4)),
-    ("pixart", lambda: CONFIGS[3].scaled_blocks(64, 3)),
-    ("flux", lambda: CONFIGS[4].scaled_blocks(32, 3)),
-    ("tiny", lambda: CONFIGS[0]),
+    ("dit", lambda: by_name("dit_xl2_256").scaled_blocks(16, 4)),
+    ("pixart", lambda: by_name("pixart_sigma_1024").scaled_blocks(64, 3)),
+    ("flux", lambda: by_name("flux_dev_1024").scaled_blocks(32, 3)),
+    ("tiny", lambda: by_name("tiny")),
 ]
 
 
@@ -80,7 +80,7 @@ def test_residual_more_segments_than_one_launch_holds():
     """300 segments over one residual: the covering list is split across
     launches that accumulate in place."""
     L = 4096
-    cfg = CONFIGS[1].with_segments([(1, 4, 1024)] * 300)
+    cfg = by_name("dit_xl2_256").with_segments([(1, 4, 1024)] * 300)
     entries, cache = _fill(cfg, cfg.nodes)
     w = cheb.cheb_precompute_weights(cache.history(), [cfg.targets[0]])[0]
     x_out = torch.empty(L, dtype=torch.float32, device="cuda")
@@ -95,7 +95,7 @@ def test_residual_more_segments_than_one_launch_holds():
 
 def test_residual_partial_coverage_and_unmapped_segments():
     """Segments covering different parts of the residual, one left out."""
-    cfg = CONFIGS[3].with_segments([(64, 8), (32, 8), (16, 8), (64, 8), (8, 8)])
+    cfg = by_name("pixart_sigma_1024").with_segments([(64, 8), (32, 8), (16, 8), (64, 8), (8, 8)])
     res_off = [0, 256, 128, 0, -1]
     L = 64 * 8
     entries, cache = _fill(cfg, cfg.nodes)
@@ -219,7 +219,7 @@ def _compact_problem(cfg, entries, res_off, res_n, seg_off, idx):
     return compact, [s * m for s in range(n_seg)], [m] * n_seg, [0] * n_seg, m
 
 
-@pytest.mark.parametrize("cfg", CONFIGS[1:], ids=lambda c: c.name)
+@pytest.mark.parametrize("cfg", [c for c in CONFIGS if c.name != "tiny"], ids=lambda c: c.name)
 def test_residual_full_size_sampled(cfg):
     res_off, res_n = cfg.residual_map()
     entries, cache = _fill(cfg, cfg.nodes)

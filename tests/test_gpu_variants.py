@@ -7,14 +7,14 @@ import torch
 
 import oracle
 import paper_2608_23429_amd as cheb
-from synth import CONFIGS, make_history, split_segments
+from synth import CONFIGS, make_history, split_segments, by_name
 from tests.gpu_util import check_parity, to_host_bits
 
 pytestmark = pytest.mark.gpu
 
 
 def test_alternating_weights_through_the_kernel():
-    cfg = CONFIGS[4].shrunk(300_000)
+    cfg = by_name("flux_dev_1024").shrunk(300_000)
     entries = make_history(cfg, "cuda")
     cache = cheb.ChebCache(cfg.n_hist, torch.bfloat16, cfg.seg_numel)
     for x, e in zip(cfg.nodes, entries):
@@ -33,7 +33,7 @@ def test_chebyshev_placed_full_steps_online():
     """Full steps at rounded Chebyshev roots of a 50-step flow schedule,
     predicted steps from the table, each checked against the oracle's
     Algorithm-1 simulation on the same mask."""
-    cfg = CONFIGS[4].shrunk(100_000)
+    cfg = by_name("flux_dev_1024").shrunk(100_000)
     T, n = 50, 4
     sigma = 1.0 - np.arange(T) / T
     steps = np.unique(np.rint(cheb.cheb_chebyshev_nodes(14, 1, 0, T - 1)).astype(int))

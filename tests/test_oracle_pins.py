@@ -14,7 +14,7 @@ import pytest
 import torch
 
 import oracle
-from synth import CONFIGS, make_history_f64
+from synth import CONFIGS, make_history_f64, by_name
 from tests.lagrange_exact import lagrange_weights
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
@@ -234,7 +234,7 @@ def test_tiny_generator_linearity():
     """Tiny workload: F_k = A + B tau_k + C tau_k^2 + 1e-3 eta_k (fp64, unrounded).
     The K=3 combination returns the quadratic at the target exactly plus the
     combined noise 1e-3 sum_k w_k eta_k."""
-    c = CONFIGS[0]
+    c = by_name("tiny")
     E = 20000
     entries, coeffs, eta, taus = make_history_f64(c, E)
     for t in list(c.targets) + list(c.alt_targets):
