@@ -243,6 +243,85 @@ def time_residual(torch, cheb, cfg, entries, cache, steps, warmup):
     }
 
 
+def time_online_run(torch, cheb, cfg, entries, reps=3):
+    """The online stage over one whole sampling run of T = 50 steps from the
+    offline table (Section 3.3 schedule with s0 = s1 = 1, r = 6, history of
+    the workload's size; steps before the history fills run in full): every
+    full step pushes its features, every run of skipped steps is predicted
+    in one pass (per-module form); and the same run with the collapsed
+    residual history (entry from the residual difference per full step, one
+    residual prediction per skipped step)."""
+    import numpy as np
+    from synth import split_segments
+    T, s0, s1, r, n = 50, 1, 1, 6, cfg.n_hist
+    x = 1.0 - np.arange(T) / 50.0 if cfg.time_scale == 1.0 else 999.0 - 20.0 * np.arange(T)
+    table = cheb.ChebTable(T, s0, s1, r, n, x, cheb.CHEB_SHORT_FULL)
+    predicted = [table.step(s)[0] for s in range(T)]
+    runs = dict(table.runs())
+    dt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    cache = cheb.ChebCache(n, dt, cfg.seg_numel)
+    outs = [cache.new_output() for _ in range(max(runs.values()))]
+    segs = [split_segments(e, cfg) for e in entries]
+    res_off, res_n = cfg.residual_map()
+    hist = cheb.ResidualHistory(n, res_off, res_n)
+    x_before = torch.randn(res_n, device="cuda")
+    x_after = torch.randn(res_n, device="cuda")
+    x_out = torch.empty_like(x_before)
+
+    def per_module():
+        cache.reset()
+        s, k = 0, 0
+        while s < T:
+            if not predicted[s]:
+                cache.push(float(x[s]), segs[k % len(segs)])
+                k += 1
+                s += 1
+            else:
+                c = runs[s]
+                cache.extrapolate_steps(table, s, c, outs[:c])
+                s += c
+
+    def collapsed():
+        hist.cache.reset()
+        for s in range(T):
+            if not predicted[s]:
+                hist.push_difference(float(x[s]), x_after, x_before)
+            else:
+                hist.predict(float(x[s]), x_out, x_before)
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        ms = []
+        for _ in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            fn()
+            b.record()
+            b.synchronize()
+            ms.append(a.elapsed_time(b))
+        return sorted(ms)[len(ms) // 2]
+
+    n_full = T - sum(predicted)
+    res = {
+        "table": f"T={T} s0={s0} s1={s1} r={r} n={n}, short history run in full",
+        "full_steps": n_full, "predicted_steps": T - n_full,
+        "per_module_ms": timed(per_module),
+        "collapsed_residual_ms": timed(collapsed),
+        "single_target_predictions_ms": None,
+        "note": "device time of the online stage for one image (pushes and predictions; "
+                "the DiT forward of the full steps is not included); "
+                "single_target_predictions_ms is the predicted steps alone at one launch "
+                "each, for comparison; not in value",
+    }
+    cache.close()
+    hist.close()
+    table.close()
+    del outs
+    torch.cuda.empty_cache()
+    return res
+
+
 def oracle_parity_sample(torch, cfg, entries, cache, out, target, count=1 << 16):
     """Part of the CPU-baseline leg: the same oracle, untimed, recomputes a
     sample of the device's prediction at `target` from the stored history."""
@@ -434,6 +513,11 @@ def main(argv=None):
     log(f"[bench] {cfg.name} multi-target: {multi['us_per_skipped_step']:.1f} us per skipped "
         f"step ({multi['gbps']:.0f} GB/s over {multi['targets_per_pass']} targets)")
     resid = time_residual(torch, cheb, cfg, entries, cache, max(10, args.steps // 2), args.warmup)
+    online = time_online_run(torch, cheb, cfg, entries)
+    online["single_target_predictions_ms"] = online["predicted_steps"] * res["us_per_step"] / 1e3
+    log(f"[bench] {cfg.name} one sampling run ({online['full_steps']} full, "
+        f"{online['predicted_steps']} predicted steps): per-module {online['per_module_ms']:.2f} ms, "
+        f"collapsed residual {online['collapsed_residual_ms']:.2f} ms")
     log(f"[bench] {cfg.name} residual: full form {resid['full_form']['us']:.1f} us, collapsed "
         f"predict {resid['collapsed_predict']['us']:.1f} us + push-time reduce "
         f"{resid['collapsed_push_reduce']['us']:.1f} us (or residual difference "
@@ -467,6 +551,7 @@ def main(argv=None):
                  "note": "full-step copy into the ring, once per full step (not in value)"},
         "multi_target": multi,
         "residual": resid,
+        "online_run": online,
     }
     if not args.no_cpu_baseline:
         log(f"[bench] oracle CPU baseline (~{args.cpu_seconds:.0f} s)")
