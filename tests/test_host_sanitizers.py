@@ -40,3 +40,28 @@ def test_host_code_under_asan_ubsan(tmp_path):
                        env=env, timeout=120)
     assert r.returncode == 0, r.stdout + r.stderr
     assert "c abi ok" in r.stdout
+
+
+@pytest.mark.skipif(shutil.which("g++") is None, reason="needs g++")
+def test_host_code_under_tsan(tmp_path):
+    """Eight threads call the host entry points at once (weights, tables,
+    launch shape, error messages, a ring handle each) in a ThreadSanitizer
+    build: no data race is reported and every result is as single-threaded."""
+    san = ["-fsanitize=thread", "-fno-omit-frame-pointer", "-g", "-O1"]
+    inc = ["-I", os.path.join(ROOT, "include"), "-I", CSRC, "-I", os.path.join(ROCM, "include")]
+    objs = []
+    for src in HOST_SOURCES + ["host_stubs.cpp", "host_threads.cpp"]:
+        path = os.path.join(HERE if src.startswith("host_") else CSRC, src)
+        obj = os.path.join(tmp_path, src + ".o")
+        subprocess.run(["g++", "-std=c++17", "-D__HIP_PLATFORM_AMD__", *san, *inc, "-c", path,
+                        "-o", obj], check=True)
+        objs.append(obj)
+    exe = os.path.join(tmp_path, "host_threads_tsan")
+    libdir = os.path.join(ROCM, "lib")
+    subprocess.run(["g++", *san, *objs, "-o", exe, "-L", libdir, "-lamdhip64",
+                    f"-Wl,-rpath,{libdir}", "-lm", "-pthread"], check=True)
+    env = dict(os.environ, TSAN_OPTIONS="halt_on_error=1:second_deadlock_stack=1")
+    r = subprocess.run([exe], capture_output=True, text=True, env=env, timeout=300)
+    assert r.returncode == 0, r.stdout + r.stderr
+    assert "threads ok" in r.stdout
+    assert "WARNING: ThreadSanitizer" not in r.stderr, r.stderr
