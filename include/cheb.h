@@ -145,7 +145,8 @@ CHEB_API int cheb_chebyshev_nodes(int32_t n, int32_t kind, double a, double b, d
  *
  *   src     [n_src] host array of device pointers, each to numel elements of
  *           `dtype`, 16-byte aligned.
- *   w       [n_src] host fp64 weights (converted to fp32 on the bf16 path).
+ *   w       [n_src] host fp64 weights, finite (converted to fp32 on the bf16
+ *           path, where a magnitude above FLT_MAX is CHEB_E_NONFINITE).
  *   out     device pointer to numel elements of `dtype`, 16-byte aligned.
  *           It may not overlap any source.
  *   numel   >= 0, below 2^34.  Any value; a ragged tail is handled.

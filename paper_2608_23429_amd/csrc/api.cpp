@@ -1,5 +1,6 @@
 // Host side of libcheb: error reporting, launch shape, weight
 // precomputation and the stateless combination entry point.
+#include <float.h>
 #include <limits.h>
 #include <math.h>
 #include <stdarg.h>
@@ -304,8 +305,12 @@ int cheb_combine_multi(const void *const *src, int32_t n_src, const double *w, i
   if (numel < 0) return fail(CHEB_E_INVAL, "numel is negative");
   if (numel / elems_per_vec(dtype) >= kMaxVecs)
     return fail(CHEB_E_INVAL, "numel %lld too large for one launch", (long long)numel);
-  for (int m = 0; m < n_out * n_src; ++m)
+  for (int m = 0; m < n_out * n_src; ++m) {
     if (!isfinite(w[m])) return fail(CHEB_E_NONFINITE, "weight %d is not finite", m);
+    // The bf16 kernel takes its weights as fp32.
+    if (dtype == CHEB_BF16 && fabs(w[m]) > double(FLT_MAX))
+      return fail(CHEB_E_NONFINITE, "weight %d (%.17g) overflows fp32", m, w[m]);
+  }
   if (numel == 0) return ok();
   const uintptr_t bytes = uintptr_t(numel) * elem_bytes(dtype);
   auto overlap = [bytes](const void *a, const void *b) {

@@ -332,6 +332,7 @@ def test_combine_validation_before_launch():
         (([a + 2, b], [0.5, 0.5], o, 100, 0), B.CHEB_E_ALIGN),
         (([a, b], [0.5, 0.5], o + 4, 100, 0), B.CHEB_E_ALIGN),
         (([a, b], [0.5, float("nan")], o, 100, 0), B.CHEB_E_NONFINITE),
+        (([a, b], [0.5, 1e39], o, 100, 0), B.CHEB_E_NONFINITE),     # past fp32 (bf16 path)
         (([a, b], [0.5, 0.5], a + 64, 100, 0), B.CHEB_E_INVAL),      # overlap
         (([a, b], [0.5, 0.5], o, -1, 0), B.CHEB_E_INVAL),
         (([a, b], [0.5, 0.5], o, 1 << 34, 0), B.CHEB_E_INVAL),
