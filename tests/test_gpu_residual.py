@@ -150,10 +150,11 @@ DIFF_TOL = 1e-4
 @pytest.mark.parametrize("case", SMALL[:3], ids=lambda c: c[0])
 def test_collapsed_history_from_residual_difference(case):
     """The collapsed entry taken as x_after - x_before of a full step's
-    block stack (ResidualHistory.push_difference), against the oracle's
-    x_in + sum_k w_k (x_after_k - x_before_k) in fp64; and, by the block
-    equation, the same entries as the push-time reduction of the module
-    outputs up to the fp32 rounding of x_after."""
+    block stack (ResidualHistory.push_difference): each entry is the
+    oracle's exact difference rounded once to fp32, bit for bit, and by the
+    block equation the oracle's sum of the step's module outputs up to the
+    fp32 rounding of x_after; the prediction against the oracle's
+    x_in + sum_k w_k (x_after_k - x_before_k) in fp64."""
     cfg = case[1]()
     res_off, res_n = cfg.residual_map()
     entries = make_history(cfg, "cuda")
@@ -172,13 +173,22 @@ def test_collapsed_history_from_residual_difference(case):
         diff.push_difference(x, xa, xb)
         red.push(x, split_segments(e, cfg))
     torch.cuda.synchronize()
-    for k in range(cfg.n_hist):
-        d = diff.cache.entry(k)[:res_n].double()
-        r = red.cache.entry(k)[:res_n].double()
-        scale = (afters[k].double().abs() + befores[k].double().abs()).max().item()
-        assert (d - r).abs().max().item() <= 4 * 2.0 ** -24 * scale, k
     hosts_a = [a.cpu().numpy() for a in afters]
     hosts_b = [b.cpu().numpy() for b in befores]
+    for k in range(cfg.n_hist):
+        d = diff.cache.entry(k)[:res_n].cpu().numpy()
+        # the entry is the exact difference rounded once to fp32: bit for bit
+        exact, _ = oracle.residual([hosts_a[k], hosts_b[k]], [1.0, -1.0], [0], [res_n], [0], res_n,
+                                   dtype="f32")
+        assert np.array_equal(d.view(np.uint32), exact.astype(np.float32).view(np.uint32)), k
+        # and, by the block equation, the sum of the step's module outputs up
+        # to the fp32 rounding of x_after
+        outs_sum, _ = oracle.residual([to_host_bits(entries[k])], [1.0], seg_off, cfg.seg_numel,
+                                      res_off, res_n)
+        scale = float((np.abs(hosts_a[k]) + np.abs(hosts_b[k])).max())
+        assert np.max(np.abs(d - outs_sum)) <= 3 * 2.0 ** -24 * scale, k
+        r = red.cache.entry(k)[:res_n].cpu().numpy()
+        assert np.max(np.abs(r - outs_sum)) <= 2.0 ** -24 * np.abs(outs_sum).max() + 1e-30, k
     x_in = _x_in(res_n, 12)
     for t in cfg.targets:
         x_out = torch.empty_like(x_in)
