@@ -1,14 +1,17 @@
 """Skipped-step predictions captured in a HIP graph (torch.cuda.CUDAGraph)
 and replayed: the library only launches kernels (no allocation, no memset),
-so captured predictions replay to the same bits as eager ones.  Every
-replay is checked, with eager work and synchronisation in between.  Pushes
+so captured predictions replay to the same bits as eager ones, which are
+checked against the oracle first.  Every replay is checked, with eager work
+and synchronisation in between.  Pushes
 are not captured: they update host-side ring state at call time."""
 import numpy as np
 import pytest
 import torch
 
+import oracle
 import paper_2608_23429_amd as cheb
 from synth import CONFIGS, make_history, split_segments, by_name
+from tests.gpu_util import check_parity, to_host_bits
 
 pytestmark = pytest.mark.gpu
 
@@ -24,6 +27,11 @@ def test_predictions_replay_from_a_graph(cfg):
     eager = [cache.extrapolate_at(t)[0].clone() for t in cfg.targets]
     eager_multi = cache.extrapolate_at_multi(cfg.targets)[0]
     torch.cuda.synchronize()
+    hosts = [to_host_bits(e) for e in entries]
+    for t, e, em in zip(cfg.targets, eager, eager_multi):
+        w = oracle.weights_row(cfg.nodes, t)
+        check_parity(to_host_bits(e), hosts, w, cfg.dtype, f"eager t={t}")
+        check_parity(to_host_bits(em), hosts, w, cfg.dtype, f"eager multi t={t}")
     outs = [cache.new_output() for _ in cfg.targets]
     outs_multi = [cache.new_output() for _ in cfg.targets]
     side = torch.cuda.Stream()

@@ -188,8 +188,10 @@ def test_fused_push_matches_copy_push(dtype):
     seg = [4096 * 8, 1000, 24]
     a = cheb.ChebCache(3, DT[dtype], seg)
     b = cheb.ChebCache(3, DT[dtype], seg)
+    pushed = []
     for i, t in enumerate([0.96, 0.9, 0.8, 0.72]):
         segs = [(_rand(1, m, dtype, seed=10 * i + k)[0]) for k, m in enumerate(seg)]
+        pushed.append(segs)
         a.push(t, segs)
         slot = b.begin_push()
         for view, src in zip(b.segment_views(slot), segs):
@@ -200,6 +202,10 @@ def test_fused_push_matches_copy_push(dtype):
     oa, _ = a.extrapolate_at(0.6)
     ob, _ = b.extrapolate_at(0.6)
     torch.cuda.synchronize()
+    w = oracle.weights_row([0.9, 0.8, 0.72], 0.6)
+    for s_idx, va in enumerate(a.segment_views(oa)):
+        check_parity(to_host_bits(va), [to_host_bits(p[s_idx]) for p in pushed[1:]], w, dtype,
+                     f"copy push segment {s_idx}")
     for va, vb in zip(a.segment_views(oa), b.segment_views(ob)):
         assert torch.equal(va.view(torch.int16 if dtype == "bf16" else torch.int32),
                            vb.view(torch.int16 if dtype == "bf16" else torch.int32))
