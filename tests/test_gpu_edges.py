@@ -121,6 +121,8 @@ def test_largest_launch(dtype):
     around the last tile and at random."""
     numel = _max_numel(dtype)
     nbytes = numel * (2 if dtype == "bf16" else 4)
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()                        # blocks cached by earlier tests
     free, _ = torch.cuda.mem_get_info()
     if free < 4 * nbytes + (8 << 30):
         pytest.skip(f"needs {4 * nbytes + (8 << 30)} free bytes, {free} free")
