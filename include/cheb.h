@@ -116,14 +116,22 @@ CHEB_API int cheb_precompute_weights(const double *hist_t, int32_t n_hist,
 enum {
   CHEB_RHO_GENERAL = 0,     /* rho_j = 1/omega'(x_j) (Appendix A): the
                                Lagrange interpolant, as cheb_precompute_weights */
-  CHEB_RHO_ALTERNATING = 1  /* rho_j = (-1)^j (1/2 at both ends, else 1), the
+  CHEB_RHO_ALTERNATING = 1, /* rho_j = (-1)^j (1/2 at both ends, else 1), the
                                weights printed in Section 3.2: exact for
                                Chebyshev extrema, a rational interpolant that
                                reproduces degree <= 1 at equispaced nodes */
+  CHEB_TAYLOR = 2           /* not a barycentric form: the Taylor expansion
+                               about the newest abscissa, the i-th derivative
+                               over i! estimated by the divided difference over
+                               the newest i+1 abscissae (the Taylor comparison
+                               of Section 3.2's Runge study); reproduces
+                               degree <= 1, and the unit row at the newest
+                               abscissa only */
 };
 
-/* cheb_precompute_weights with a choice of barycentric weights rho_j in the
- * coefficient equation of Section 3.2.  Arguments and errors as
+/* cheb_precompute_weights with a choice of coefficient generator: the
+ * barycentric weights rho_j of the coefficient equation of Section 3.2, or
+ * the Taylor expansion above.  Arguments and errors as
  * cheb_precompute_weights, plus CHEB_E_INVAL for an unknown variant. */
 CHEB_API int cheb_precompute_weights_variant(const double *hist_t, int32_t n_hist,
                                              const double *target_t, int32_t n_target,

@@ -81,6 +81,8 @@ def bind(path):
                                          ctypes.c_double, _c_double_p]
     L.oracle_weights_row_alternating.argtypes = [_c_double_p, ctypes.c_int, ctypes.c_double,
                                                  _c_double_p]
+    L.oracle_weights_row_taylor.argtypes = [_c_double_p, ctypes.c_int, ctypes.c_double,
+                                            _c_double_p]
     _i64 = ctypes.POINTER(ctypes.c_int64)
     L.oracle_residual_bf16.argtypes = [ctypes.POINTER(_c_u16_p), ctypes.c_int, _c_double_p,
                                        _i64, _i64, _i64, ctypes.c_int, _c_double_p,
@@ -353,4 +355,15 @@ def weights_row_alternating(x, xstar):
     w = np.empty_like(x)
     _check(lib().oracle_weights_row_alternating(_ptr(x, ctypes.c_double), len(x), float(xstar),
                                                 _ptr(w, ctypes.c_double)))
+    return w
+
+
+def weights_row_taylor(x, xstar):
+    """Coefficients of the Taylor expansion about the newest node with
+    divided-difference derivative estimates (the Taylor comparison of
+    Section 3.2's Runge study)."""
+    x = _f64(x)
+    w = np.empty_like(x)
+    _check(lib().oracle_weights_row_taylor(_ptr(x, ctypes.c_double), len(x), float(xstar),
+                                           _ptr(w, ctypes.c_double)))
     return w

@@ -460,3 +460,33 @@ int oracle_weights_row_alternating(const double *x, int n, double xstar, double 
   for (int j = 0; j < n; ++j) w[j] /= denom;
   return 0;
 }
+
+/* Taylor expansion about the newest node x_{n-1} (the comparison of
+ * Section 3.2's Runge-function study, whose text gives no formula; the
+ * reading taken here): the i-th derivative over i! is estimated by the
+ * divided difference over the newest i+1 nodes, so
+ *     P(x*) = sum_{i=0}^{n-1} f[x_{n-1}, ..., x_{n-1-i}] (x* - x_{n-1})^i.
+ * On equispaced nodes f[...] is the i-th backward difference over i! h^i.
+ * The coefficient of every f_j comes from the recursive divided-difference
+ * table run on the unit vector e_j.  Returns 0 or a negative code. */
+int oracle_weights_row_taylor(const double *x, int n, double xstar, double *w) {
+  int rc = oracle_check_nodes(x, n);
+  if (rc) return rc;
+  if (!isfinite(xstar)) return -2;
+  if (n > ORACLE_MAX_NODES) return -1;
+  const double d = xstar - x[n - 1];
+  for (int j = 0; j < n; ++j) {
+    /* table[k] holds the divided difference over nodes k-i .. k of e_j */
+    double table[ORACLE_MAX_NODES];
+    for (int k = 0; k < n; ++k) table[k] = (k == j) ? 1.0 : 0.0;
+    double sum = table[n - 1];     /* i = 0: f[x_{n-1}] */
+    double power = 1.0;
+    for (int i = 1; i < n; ++i) {
+      for (int k = n - 1; k >= i; --k) table[k] = (table[k] - table[k - 1]) / (x[k] - x[k - i]);
+      power *= d;
+      sum += table[n - 1] * power;
+    }
+    w[j] = sum;
+  }
+  return 0;
+}

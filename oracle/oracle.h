@@ -51,6 +51,7 @@ int oracle_table_row(int T, int s0, int s1, int r, int n, const double *abscissa
 
 int oracle_chebyshev_nodes(int n, int kind, double a, double b, double *x);
 int oracle_weights_row_alternating(const double *x, int n, double xstar, double *w);
+int oracle_weights_row_taylor(const double *x, int n, double xstar, double *w);
 int oracle_residual_bf16(const uint16_t *const *F, int n, const double *w,
                          const int64_t *slot_offset, const int64_t *seg_numel,
                          const int64_t *res_offset, int n_segs, const double *x_in,

@@ -14,7 +14,7 @@ import torch
 
 from ._binding import (  # noqa: F401  (re-exported C entry points)
     CHEB_BF16, CHEB_F32, CHEB_MAX_NODES, CHEB_MAX_OUTPUTS, CHEB_MAX_SLOTS, CHEB_RHO_ALTERNATING,
-    CHEB_RHO_GENERAL, CHEB_SHORT_FULL, CHEB_SHORT_LOWER, ChebError, cheb_chebyshev_nodes,
+    CHEB_RHO_GENERAL, CHEB_SHORT_FULL, CHEB_TAYLOR, CHEB_SHORT_LOWER, ChebError, cheb_chebyshev_nodes,
     cheb_precompute_weights_variant,
     cheb_cache_begin_push, cheb_cache_commit, cheb_cache_create, cheb_cache_destroy,
     cheb_cache_dtype, cheb_cache_entry, cheb_cache_history, cheb_cache_layout, cheb_cache_push,

@@ -28,6 +28,7 @@ CHEB_SHORT_LOWER = 1
 
 CHEB_RHO_GENERAL = 0
 CHEB_RHO_ALTERNATING = 1
+CHEB_TAYLOR = 2
 
 CHEB_BF16 = 0
 CHEB_F32 = 1

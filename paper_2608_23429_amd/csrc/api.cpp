@@ -197,6 +197,40 @@ int weights_row_alternating(const double *x, int n, double target, double *w) {
   return check_row(w, n, target);
 }
 
+// Taylor expansion about the newest abscissa x_{n-1} (the comparison in
+// Section 3.2's Runge-function study; the text gives no formula): the i-th
+// derivative over i! is estimated by the divided difference over the newest
+// i + 1 abscissae,
+//     P(t) = sum_{i<n} f[x_{n-1-i}, ..., x_{n-1}] (t - x_{n-1})^i,
+// and the divided difference over the set S is sum_{j in S} f_j / prod_{m in
+// S, m != j} (x_j - x_m).  On equispaced abscissae it is the i-th backward
+// difference over i! h^i.
+int weights_row_taylor(const double *x, int n, double target, double *w) {
+  if (n < 1 || n > CHEB_MAX_NODES)
+    return fail(CHEB_E_INVAL, "history size %d outside 1..%d", n, CHEB_MAX_NODES);
+  if (!isfinite(target)) return fail(CHEB_E_NONFINITE, "target abscissa is not finite");
+  for (int j = 0; j < n; ++j) {
+    if (!isfinite(x[j])) return fail(CHEB_E_NONFINITE, "history abscissa %d is not finite", j);
+    for (int k = 0; k < j; ++k)
+      if (x[j] == x[k])
+        return fail(CHEB_E_DUPNODE, "history abscissae %d and %d are equal (%.17g)", k, j, x[j]);
+  }
+  for (int j = 0; j < n; ++j) w[j] = 0.0;
+  const double d = target - x[n - 1];
+  double power = 1.0;  // d^i
+  for (int i = 0; i < n; ++i) {
+    const int first = n - 1 - i;
+    for (int j = first; j < n; ++j) {
+      double den = 1.0;
+      for (int m = first; m < n; ++m)
+        if (m != j) den *= x[j] - x[m];
+      w[j] += power / den;
+    }
+    power *= d;
+  }
+  return check_row(w, n, target);
+}
+
 }  // namespace cheb
 
 using namespace cheb;
@@ -260,21 +294,23 @@ int cheb_precompute_weights_variant(const double *hist_t, int32_t n_hist,
                                     double *w_out) {
   if (variant == CHEB_RHO_GENERAL)
     return cheb_precompute_weights(hist_t, n_hist, target_t, n_target, w_out);
-  if (variant != CHEB_RHO_ALTERNATING) return fail(CHEB_E_INVAL, "unknown weight variant %d", variant);
+  if (variant != CHEB_RHO_ALTERNATING && variant != CHEB_TAYLOR)
+    return fail(CHEB_E_INVAL, "unknown weight variant %d", variant);
+  auto row_of = variant == CHEB_TAYLOR ? weights_row_taylor : weights_row_alternating;
   if (!hist_t) return fail(CHEB_E_INVAL, "hist_t is NULL");
   if (n_target < 0) return fail(CHEB_E_INVAL, "n_target is negative");
   if (n_target > 0 && (!target_t || !w_out)) return fail(CHEB_E_INVAL, "target_t or w_out is NULL");
   double row[CHEB_MAX_NODES];
   for (int32_t m = 0; m < n_target; ++m) {
-    int rc = weights_row_alternating(hist_t, n_hist, target_t[m], row);
+    int rc = row_of(hist_t, n_hist, target_t[m], row);
     if (rc != CHEB_OK) return rc;
   }
   if (n_target == 0) {
-    int rc = weights_row_alternating(hist_t, n_hist, hist_t[0], row);
+    int rc = row_of(hist_t, n_hist, hist_t[0], row);
     if (rc != CHEB_OK) return rc;
   }
   for (int32_t m = 0; m < n_target; ++m) {
-    weights_row_alternating(hist_t, n_hist, target_t[m], row);
+    row_of(hist_t, n_hist, target_t[m], row);
     memcpy(w_out + size_t(m) * n_hist, row, sizeof(double) * n_hist);
   }
   return ok();

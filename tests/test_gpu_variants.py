@@ -1,6 +1,7 @@
 """Weight variants on the device path: the same kernel with the alternating
-weights printed in Section 3.2, and a table whose full steps sit at rounded
-Chebyshev points, against the oracle."""
+weights printed in Section 3.2 and with the finite-difference Taylor
+expansion, and a table whose full steps sit at rounded Chebyshev points,
+against the oracle."""
 import numpy as np
 import pytest
 import torch
@@ -26,6 +27,24 @@ def test_alternating_weights_through_the_kernel():
     for m, t in enumerate(cfg.targets):
         check_parity(to_host_bits(outs[m]), hosts, oracle.weights_row_alternating(cfg.nodes, t),
                      "bf16", f"alternating t={t}")
+    cache.close()
+
+
+@pytest.mark.parametrize("name", ["dit_xl2_256", "flux_dev_1024", "tiny"])
+def test_taylor_weights_through_the_kernel(name):
+    cfg = by_name(name).shrunk(300_000)
+    dt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    entries = make_history(cfg, "cuda")
+    cache = cheb.ChebCache(cfg.n_hist, dt, cfg.seg_numel)
+    for x, e in zip(cfg.nodes, entries):
+        cache.push(x, split_segments(e, cfg))
+    w = cheb.cheb_precompute_weights_variant(cfg.nodes, cfg.targets, cheb.CHEB_TAYLOR)
+    outs = cache.extrapolate_multi(w)
+    torch.cuda.synchronize()
+    hosts = [to_host_bits(e) for e in entries]
+    for m, t in enumerate(cfg.targets):
+        check_parity(to_host_bits(outs[m]), hosts, oracle.weights_row_taylor(cfg.nodes, t),
+                     cfg.dtype, f"{name} taylor t={t}")
     cache.close()
 
 

@@ -58,6 +58,11 @@ MUTANTS = [
      "((j == 0) ? 0.5 : 1.0)", 0),
     ("alternating weights without sign", "double rho = ((j % 2) ? -1.0 : 1.0)", "double rho = ((j % 2) ? 1.0 : 1.0)", 0),
     ("Chebyshev roots shifted", "cos((2.0 * j - 1.0) * pi / (2.0 * n))", "cos((2.0 * j) * pi / (2.0 * n))", 0),
+    ("Taylor about the oldest node", "const double d = xstar - x[n - 1];", "const double d = xstar - x[0];", 0),
+    ("Taylor divided difference over adjacent nodes only",
+     "(table[k] - table[k - 1]) / (x[k] - x[k - i])", "(table[k] - table[k - 1]) / (x[k] - x[k - 1])", 0),
+    ("Taylor drops the top order", "for (int i = 1; i < n; ++i) {\n      for (int k = n - 1; k >= i; --k)",
+     "for (int i = 1; i < n - 1; ++i) {\n      for (int k = n - 1; k >= i; --k)", 0),
     ("table uses step not abscissa", "return oracle_weights_row(x, count, abscissa[s], w);",
      "return oracle_weights_row(x, count, abscissa[s] + 1.0, w);", 0),
 ]

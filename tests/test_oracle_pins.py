@@ -490,6 +490,62 @@ def test_alternating_weights_at_equispaced_nodes_reproduce_degree_one_only():
     assert oracle.weights_row_alternating(x, x[2]).tolist() == [0, 0, 1, 0, 0, 0]
 
 
+def _taylor_by_backward_differences(x, t):
+    """Textbook finite-difference Taylor polynomial about the newest of
+    equispaced nodes, sum_i (nabla^i f)_newest / (i! h^i) (t - x_newest)^i,
+    with the backward differences taken by numpy on each unit vector."""
+    n = len(x)
+    h = x[1] - x[0] if n > 1 else 1.0
+    d = t - x[-1]
+    w = np.zeros(n)
+    for j in range(n):
+        e = np.zeros(n)
+        e[j] = 1.0
+        w[j] = sum((np.diff(e, i)[-1] if i else e[-1]) / (math.factorial(i) * h ** i) * d ** i
+                   for i in range(n))
+    return w
+
+
+def test_taylor_weights_equal_finite_difference_taylor_on_equispaced_nodes():
+    for n in range(1, 9):
+        for x0, h in [(0.0, 1.0), (999.0, -20.0), (0.96, -0.02), (-1.0, 2.0 / 7.0)]:
+            x = x0 + h * np.arange(n)
+            for t in (x[-1] + h, x[-1] + 2.5 * h, x[-1] - 0.5 * h, x[0]):
+                got = oracle.weights_row_taylor(x, t)
+                want = _taylor_by_backward_differences(x, t)
+                assert np.max(np.abs(got - want)) <= 1e-12 * max(1.0, np.abs(want).sum()), (n, h, t)
+
+
+def test_taylor_weights_closed_forms():
+    """Any distinct nodes: constants and lines are reproduced; for f = x^2
+    the expansion misses by exactly (t - x_K)(x_{K-1} - x_K) once three or
+    more nodes are held; the newest node gets the unit row; two nodes give
+    the Lagrange (linear) row; an affine map of nodes and target changes
+    nothing."""
+    rng = np.random.default_rng(47)
+    for _ in range(200):
+        n = int(rng.integers(1, 9))
+        x = np.sort(rng.uniform(-3.0, 3.0, n))[::-1] if rng.random() < 0.5 else rng.uniform(-3.0, 3.0, n)
+        if len(set(x.tolist())) < n or (n > 1 and np.min(np.abs(np.subtract.outer(x, x)) + np.eye(n)) < 0.05):
+            continue
+        t = float(rng.uniform(-5.0, 5.0))
+        w = oracle.weights_row_taylor(x, t)
+        scale = max(1.0, np.abs(w).sum())
+        assert abs(w.sum() - 1.0) <= 1e-11 * scale
+        if n >= 2:
+            assert abs(w @ x - t) <= 1e-11 * scale * max(1.0, np.abs(x).max(), abs(t))
+        if n >= 3:
+            miss = w @ (x * x) - t * t
+            want = (t - x[-1]) * (x[-2] - x[-1])
+            assert abs(miss - want) <= 1e-10 * scale * max(1.0, np.abs(x).max(), abs(t)) ** 2, (n, miss, want)
+        assert oracle.weights_row_taylor(x, x[-1]).tolist() == [0.0] * (n - 1) + [1.0]
+        if n == 2:
+            np.testing.assert_allclose(w, oracle.weights_row(x, t), rtol=0, atol=1e-12 * scale)
+        a, b = 3.5, -1.25
+        np.testing.assert_allclose(oracle.weights_row_taylor(a * x + b, a * t + b), w,
+                                   rtol=0, atol=1e-10 * scale)
+
+
 def test_table_mask_of_schedule_equals_schedule_rows():
     x = 999.0 - 37.0 * np.arange(20)
     mask = oracle.full_schedule(20, 2, 1, 4)
