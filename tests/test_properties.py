@@ -90,3 +90,19 @@ def test_table_agrees_with_algorithm_one(T, s0, s1, r, n, policy):
         assert pred == bool(kind) and nodes == onodes
         if pred:
             assert np.max(np.abs(w - ow)) <= 64 * n * 2.0 ** -53 * _cond(ow)
+
+
+@SETTINGS
+@given(nodes=nodes_st, t=st.floats(-3e3, 3e3, allow_nan=False, allow_infinity=False))
+def test_taylor_weights_agree_with_oracle(nodes, t):
+    """The Taylor-style row (explicit divided-difference products in the
+    library, the recursive divided-difference table in the oracle)."""
+    ref = oracle.weights_row_taylor(nodes, t)
+    mass = float(np.abs(ref).sum())
+    try:
+        w = cheb.cheb_precompute_weights_variant(nodes, [t], cheb.CHEB_TAYLOR)[0]
+    except cheb.ChebError as e:
+        assert e.code == B.CHEB_E_NONFINITE
+        assert not np.isfinite(mass) or len(nodes) * 2.0 ** -53 * mass > LIMIT / 2
+        return
+    assert np.max(np.abs(w - ref)) <= 64 * len(nodes) * 2.0 ** -53 * _cond(ref) + 1e-300
