@@ -245,6 +245,13 @@ CHEB_API int cheb_cache_begin_push(cheb_cache *c, void **slot_base);
  * CHEB_E_DUPNODE, CHEB_E_NOTREADY (no push open). */
 CHEB_API int cheb_cache_commit(cheb_cache *c, double t);
 
+/* Fused push, abandoned: closes the open push without recording an entry
+ * (for a full step that failed before its outputs were complete).  The
+ * entry that slot held stays dropped, so a full ring holds one entry fewer
+ * afterwards; the others are untouched.  Errors: CHEB_E_INVAL,
+ * CHEB_E_NOTREADY (no push open). */
+CHEB_API int cheb_cache_abort_push(cheb_cache *c);
+
 /* Abscissae held, oldest to newest: t_out[0 .. *count-1] (t_out has room for
  * n_slots values; it may be NULL).  Errors: CHEB_E_INVAL. */
 CHEB_API int cheb_cache_history(const cheb_cache *c, double *t_out, int32_t *count);

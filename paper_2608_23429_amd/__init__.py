@@ -16,7 +16,8 @@ from ._binding import (  # noqa: F401  (re-exported C entry points)
     CHEB_BF16, CHEB_F32, CHEB_MAX_NODES, CHEB_MAX_OUTPUTS, CHEB_MAX_SLOTS, CHEB_RHO_ALTERNATING,
     CHEB_RHO_GENERAL, CHEB_SHORT_FULL, CHEB_TAYLOR, CHEB_SHORT_LOWER, ChebError, cheb_chebyshev_nodes,
     cheb_precompute_weights_variant,
-    cheb_cache_begin_push, cheb_cache_commit, cheb_cache_create, cheb_cache_destroy,
+    cheb_cache_abort_push, cheb_cache_begin_push, cheb_cache_commit, cheb_cache_create,
+    cheb_cache_destroy,
     cheb_cache_dtype, cheb_cache_entry, cheb_cache_history, cheb_cache_layout, cheb_cache_push,
     cheb_cache_reset, cheb_cache_segment_offset, cheb_cache_slot_numel, cheb_combine,
     cheb_combine_multi, cheb_extrapolate, cheb_extrapolate_at, cheb_extrapolate_at_multi,
@@ -182,7 +183,7 @@ class ResidualHistory:
         try:
             residual_reduce(segments, self.res_offset, slot[:self.res_numel], stream=stream)
         except Exception:
-            self.cache.reset()
+            self.cache.abort_push()
             raise
         self.cache.commit(t)
 
@@ -202,7 +203,7 @@ class ResidualHistory:
         try:
             combine([x_after, x_before], [1.0, -1.0], slot[:self.res_numel], stream=stream)
         except Exception:
-            self.cache.reset()
+            self.cache.abort_push()
             raise
         self.cache.commit(t)
 
@@ -301,6 +302,11 @@ class ChebCache:
 
     def commit(self, t: float):
         cheb_cache_commit(self._h, t)
+
+    def abort_push(self):
+        """Close an open fused push without recording an entry; the entry
+        its slot held stays dropped."""
+        cheb_cache_abort_push(self._h)
 
     def reset(self):
         cheb_cache_reset(self._h)

@@ -85,6 +85,7 @@ SIGNATURES = {
     "cheb_cache_push": [_vp, ctypes.c_double, _vpp, _vp],
     "cheb_cache_begin_push": [_vp, _vpp],
     "cheb_cache_commit": [_vp, ctypes.c_double],
+    "cheb_cache_abort_push": [_vp],
     "cheb_cache_history": [_vp, _dp, _i32p],
     "cheb_cache_entry": [_vp, ctypes.c_int32, _vpp],
     "cheb_cache_segment_offset": [_vp, ctypes.c_int32, _i64p],
@@ -238,6 +239,10 @@ def cheb_cache_begin_push(handle) -> int:
 
 def cheb_cache_commit(handle, t):
     _check(LIB.cheb_cache_commit(handle, float(t)))
+
+
+def cheb_cache_abort_push(h):
+    _check(LIB.cheb_cache_abort_push(h))
 
 
 def cheb_cache_history(handle, n_slots=CHEB_MAX_SLOTS):

@@ -237,6 +237,13 @@ int cheb_cache_commit(cheb_cache *c, double t) {
   return ok();
 }
 
+int cheb_cache_abort_push(cheb_cache *c) {
+  if (!c) return fail(CHEB_E_INVAL, "cache is NULL");
+  if (!c->push_open) return fail(CHEB_E_NOTREADY, "no fused push is open");
+  c->push_open = false;  // claim_slot already dropped the slot's old entry
+  return ok();
+}
+
 int cheb_cache_history(const cheb_cache *c, double *t_out, int32_t *count) {
   if (!c || !count) return fail(CHEB_E_INVAL, "cache or count is NULL");
   *count = c->count;

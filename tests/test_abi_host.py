@@ -279,6 +279,33 @@ def test_not_ready_until_full_and_while_push_open():
     cheb.cheb_cache_destroy(h)
 
 
+def test_abort_push_keeps_the_other_entries():
+    """An abandoned fused push records nothing; on a full ring the entry its
+    slot held stays dropped, every other entry stays, and the ring goes on."""
+    h, _ = _fake_cache(n_slots=3)
+    with pytest.raises(cheb.ChebError) as e:
+        cheb.cheb_cache_abort_push(h)
+    assert e.value.code == B.CHEB_E_NOTREADY
+    first = cheb.cheb_cache_begin_push(h)
+    cheb.cheb_cache_abort_push(h)                     # not full: nothing changes
+    assert cheb.cheb_cache_history(h).tolist() == []
+    assert cheb.cheb_cache_begin_push(h) == first     # the same slot again
+    cheb.cheb_cache_commit(h, 1.0)
+    for t in (2.0, 3.0):
+        cheb.cheb_cache_begin_push(h)
+        cheb.cheb_cache_commit(h, t)
+    slots = [cheb.cheb_cache_entry(h, k) for k in range(3)]
+    oldest_slot = cheb.cheb_cache_begin_push(h)
+    assert oldest_slot == slots[0]
+    cheb.cheb_cache_abort_push(h)
+    assert cheb.cheb_cache_history(h).tolist() == [2.0, 3.0]
+    assert [cheb.cheb_cache_entry(h, k) for k in range(2)] == slots[1:]
+    assert cheb.cheb_cache_begin_push(h) == oldest_slot
+    cheb.cheb_cache_commit(h, 1.5)                    # 1.0 is gone, so any value but 2, 3
+    assert cheb.cheb_cache_history(h).tolist() == [2.0, 3.0, 1.5]
+    cheb.cheb_cache_destroy(h)
+
+
 def test_duplicate_abscissa_rules():
     h, _ = _fake_cache(n_slots=3)
     for t in [10.0, 20.0, 30.0]:
