@@ -73,7 +73,10 @@ typedef enum cheb_status {
   CHEB_E_IO = -9         /* table file cannot be read or written, or is malformed */
 } cheb_status;
 
-typedef enum cheb_dtype { CHEB_BF16 = 0, CHEB_F32 = 1 } cheb_dtype;
+/* Storage types of history entries and outputs.  bf16 and fp16 are
+ * accumulated in fp32 with fp32 weights and rounded to nearest-even once;
+ * fp32 is accumulated in fp64 with fp64 weights. */
+typedef enum cheb_dtype { CHEB_BF16 = 0, CHEB_F32 = 1, CHEB_F16 = 2 } cheb_dtype;
 
 /* Message for the last failed call on this thread ("" if none).  The
  * pointer stays valid until the next failing call on the same thread. */

@@ -68,6 +68,18 @@ def bind(path):
                                           _c_double_p, ctypes.c_int64,
                                           _c_double_p, _c_double_p]
     L.oracle_extrapolate_bf16.restype = None
+    L.oracle_f16_to_f64.argtypes = [ctypes.c_uint16]
+    L.oracle_f16_to_f64.restype = ctypes.c_double
+    L.oracle_round_f16.argtypes = [ctypes.c_double]
+    L.oracle_round_f16.restype = ctypes.c_uint16
+    L.oracle_decode_f16.argtypes = [_c_u16_p, ctypes.c_int64, _c_double_p]
+    L.oracle_decode_f16.restype = None
+    L.oracle_encode_f16.argtypes = [_c_double_p, ctypes.c_int64, _c_u16_p]
+    L.oracle_encode_f16.restype = None
+    L.oracle_extrapolate_f16.argtypes = [ctypes.POINTER(_c_u16_p), ctypes.c_int,
+                                         _c_double_p, ctypes.c_int64,
+                                         _c_double_p, _c_double_p]
+    L.oracle_extrapolate_f16.restype = None
     L.oracle_extrapolate_f32.argtypes = [ctypes.POINTER(_c_f32_p), ctypes.c_int,
                                          _c_double_p, ctypes.c_int64,
                                          _c_double_p, _c_double_p]
@@ -90,6 +102,7 @@ def bind(path):
     L.oracle_residual_f32.argtypes = [ctypes.POINTER(_c_f32_p), ctypes.c_int, _c_double_p,
                                       _i64, _i64, _i64, ctypes.c_int, _c_double_p,
                                       ctypes.c_int64, _c_double_p, _c_double_p]
+    L.oracle_residual_f16.argtypes = L.oracle_residual_bf16.argtypes
     _ip = ctypes.POINTER(ctypes.c_int)
     L.oracle_table_row_mask.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_uint8), ctypes.c_int,
                                         _c_double_p, ctypes.c_int, ctypes.c_int, _ip, _ip, _ip,
@@ -184,6 +197,22 @@ def round_bf16(v):
     return out
 
 
+def f16_to_f64(h):
+    """Exact values of binary16 bit patterns (uint16 arrays)."""
+    h = np.ascontiguousarray(h, dtype=np.uint16).reshape(-1)
+    out = np.empty(h.shape, dtype=np.float64)
+    lib().oracle_decode_f16(_ptr(h, ctypes.c_uint16), h.size, _ptr(out, ctypes.c_double))
+    return out
+
+
+def round_f16(v):
+    """Correctly rounded (ties-to-even) binary16 bit patterns of fp64 values."""
+    v = _f64(v).reshape(-1)
+    out = np.empty(v.shape, dtype=np.uint16)
+    lib().oracle_encode_f16(_ptr(v, ctypes.c_double), v.size, _ptr(out, ctypes.c_uint16))
+    return out
+
+
 def _slots(slots, dtype):
     arrs = [np.ascontiguousarray(s, dtype=dtype).reshape(-1) for s in slots]
     if not arrs:
@@ -206,6 +235,21 @@ def extrapolate_bf16(slots, w, want_absmag=True):
     lib().oracle_extrapolate_bf16(ptrs, len(arrs), _ptr(w, ctypes.c_double), count,
                                   _ptr(out, ctypes.c_double),
                                   _ptr(mag, ctypes.c_double) if want_absmag else None)
+    return (out, mag) if want_absmag else out
+
+
+def extrapolate_f16(slots, w, want_absmag=True):
+    """fp64 sum_k w[k] * F_k over binary16 bit patterns (uint16 arrays)."""
+    arrs, count = _slots(slots, np.uint16)
+    w = _f64(w)
+    if len(w) != len(arrs):
+        raise OracleError("weight count differs from history size")
+    ptrs = (_c_u16_p * len(arrs))(*[_ptr(a, ctypes.c_uint16) for a in arrs])
+    out = np.empty(count, dtype=np.float64)
+    mag = np.empty(count, dtype=np.float64) if want_absmag else None
+    lib().oracle_extrapolate_f16(ptrs, len(arrs), _ptr(w, ctypes.c_double), count,
+                                 _ptr(out, ctypes.c_double),
+                                 _ptr(mag, ctypes.c_double) if want_absmag else None)
     return (out, mag) if want_absmag else out
 
 
@@ -312,9 +356,11 @@ def residual(slots, w, slot_offset, seg_numel, res_offset, res_numel, x_in=None,
              dtype="bf16"):
     """x_in + sum over mapped segments of the predicted module outputs (fp64),
     and the magnitude of its terms.  slots: history entries (uint16 patterns
-    for bf16, float32 for f32); res_offset[s] < 0 leaves segment s out."""
-    ctype = ctypes.c_uint16 if dtype == "bf16" else ctypes.c_float
-    np_t = np.uint16 if dtype == "bf16" else np.float32
+    for bf16 and f16, float32 for f32); res_offset[s] < 0 leaves segment s
+    out."""
+    half = dtype in ("bf16", "f16")
+    ctype = ctypes.c_uint16 if half else ctypes.c_float
+    np_t = np.uint16 if half else np.float32
     arrs = [np.ascontiguousarray(a, dtype=np_t).reshape(-1) for a in slots]
     w = _f64(w)
     if len(w) != len(arrs):
@@ -330,7 +376,8 @@ def residual(slots, w, slot_offset, seg_numel, res_offset, res_numel, x_in=None,
     mag = np.empty(int(res_numel), dtype=np.float64)
     P = ctypes.POINTER(ctype)
     ptrs = (P * len(arrs))(*[_ptr(a, ctype) for a in arrs])
-    fn = lib().oracle_residual_bf16 if dtype == "bf16" else lib().oracle_residual_f32
+    fn = {"bf16": lib().oracle_residual_bf16, "f16": lib().oracle_residual_f16,
+          "f32": lib().oracle_residual_f32}[dtype]
     rc = fn(ptrs, len(arrs), _ptr(w, ctypes.c_double), _ptr(so, ctypes.c_int64),
             _ptr(sn, ctypes.c_int64), _ptr(ro, ctypes.c_int64), len(sn),
             None if xi is None else _ptr(xi, ctypes.c_double), int(res_numel),

@@ -490,3 +490,105 @@ int oracle_weights_row_taylor(const double *x, int n, double xstar, double *w) {
   }
   return 0;
 }
+
+/* ------------------------------------------------------------------------ */
+/* IEEE-754 binary16 storage (the same prediction for fp16-stored caches).    */
+/* ------------------------------------------------------------------------ */
+
+/* Exact value of a binary16 pattern: 1 sign bit, 5 exponent bits (bias 15),
+ * 10 fraction bits; exponent 0 holds zero and the subnormals m * 2^-24,
+ * exponent 31 holds the infinities and NaNs. */
+double oracle_f16_to_f64(uint16_t h) {
+  const int sign = (h >> 15) & 1;
+  const int expo = (h >> 10) & 0x1F;
+  const int frac = h & 0x3FF;
+  double v;
+  if (expo == 0) {
+    v = ldexp((double)frac, -24);
+  } else if (expo == 31) {
+    v = frac ? NAN : INFINITY;
+  } else {
+    v = ldexp((double)(1024 + frac), expo - 25);
+  }
+  return sign ? -v : v;
+}
+
+/* Nearest binary16 value, ties to even; magnitudes that round to 2^16 or
+ * more become infinity; NaN becomes the quiet NaN 0x7E00. */
+uint16_t oracle_round_f16(double v) {
+  if (isnan(v)) return (uint16_t)0x7E00;
+  const uint16_t sign = signbit(v) ? 0x8000 : 0x0000;
+  const double a = fabs(v);
+  if (a == 0.0) return sign;
+  if (isinf(a)) return (uint16_t)(sign | 0x7C00);
+  int ex;
+  (void)frexp(a, &ex);                     /* a in [2^(ex-1), 2^ex) */
+  const int e = ex - 1;
+  const int qexp = (e < -14) ? -24 : e - 10;   /* spacing of binary16 there */
+  const double units = ldexp(a, -qexp);    /* exact */
+  double r = floor(units);
+  const double frac = units - r;           /* exact */
+  if (frac > 0.5 || (frac == 0.5 && fmod(r, 2.0) != 0.0)) r += 1.0;
+  const double rounded = ldexp(r, qexp);
+  if (rounded >= 65536.0) return (uint16_t)(sign | 0x7C00);
+  if (rounded < ldexp(1.0, -14)) return (uint16_t)(sign | (uint16_t)ldexp(rounded, 24));
+  int ex2;
+  (void)frexp(rounded, &ex2);
+  const int e2 = ex2 - 1;
+  const uint16_t mant = (uint16_t)((ldexp(rounded, -e2) - 1.0) * 1024.0);
+  return (uint16_t)(sign | (uint16_t)((e2 + 15) << 10) | mant);
+}
+
+void oracle_decode_f16(const uint16_t *h, int64_t count, double *out) {
+  for (int64_t i = 0; i < count; ++i) out[i] = oracle_f16_to_f64(h[i]);
+}
+
+void oracle_encode_f16(const double *v, int64_t count, uint16_t *out) {
+  for (int64_t i = 0; i < count; ++i) out[i] = oracle_round_f16(v[i]);
+}
+
+/* Section 3.3 forward application over binary16 history entries, as
+ * oracle_extrapolate_bf16. */
+void oracle_extrapolate_f16(const uint16_t *const *F, int n, const double *w,
+                            int64_t count, double *out, double *absmag) {
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < count; ++i) {
+    double s = 0.0, m = 0.0;
+    for (int k = 0; k < n; ++k) {
+      double f = oracle_f16_to_f64(F[k][i]);
+      s += w[k] * f;
+      m += fabs(w[k]) * fabs(f);
+    }
+    out[i] = s;
+    if (absmag) absmag[i] = m;
+  }
+}
+
+/* Residual application over binary16 history entries, as
+ * oracle_residual_bf16. */
+int oracle_residual_f16(const uint16_t *const *F, int n, const double *w,
+                        const int64_t *slot_offset, const int64_t *seg_numel,
+                        const int64_t *res_offset, int n_segs, const double *x_in,
+                        int64_t res_numel, double *x_out, double *absmag) {
+  for (int s = 0; s < n_segs; ++s)
+    if (res_offset[s] >= 0 && res_offset[s] + seg_numel[s] > res_numel) return -1;
+  for (int64_t j = 0; j < res_numel; ++j) {
+    x_out[j] = x_in ? x_in[j] : 0.0;
+    if (absmag) absmag[j] = x_in ? fabs(x_in[j]) : 0.0;
+  }
+  for (int s = 0; s < n_segs; ++s) {
+    if (res_offset[s] < 0) continue;
+#pragma omp parallel for schedule(static)
+    for (int64_t e = 0; e < seg_numel[s]; ++e) {
+      double acc = 0.0, mag = 0.0;
+      for (int k = 0; k < n; ++k) {
+        double f = oracle_f16_to_f64(F[k][slot_offset[s] + e]);
+        acc += w[k] * f;
+        mag += fabs(w[k]) * fabs(f);
+      }
+      x_out[res_offset[s] + e] += acc;
+      if (absmag) absmag[res_offset[s] + e] += mag;
+    }
+  }
+  return 0;
+}

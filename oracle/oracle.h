@@ -56,6 +56,16 @@ int oracle_residual_bf16(const uint16_t *const *F, int n, const double *w,
                          const int64_t *slot_offset, const int64_t *seg_numel,
                          const int64_t *res_offset, int n_segs, const double *x_in,
                          int64_t res_numel, double *x_out, double *absmag);
+double oracle_f16_to_f64(uint16_t h);
+uint16_t oracle_round_f16(double v);
+void oracle_decode_f16(const uint16_t *h, int64_t count, double *out);
+void oracle_encode_f16(const double *v, int64_t count, uint16_t *out);
+void oracle_extrapolate_f16(const uint16_t *const *F, int n, const double *w,
+                            int64_t count, double *out, double *absmag);
+int oracle_residual_f16(const uint16_t *const *F, int n, const double *w,
+                        const int64_t *slot_offset, const int64_t *seg_numel,
+                        const int64_t *res_offset, int n_segs, const double *x_in,
+                        int64_t res_numel, double *x_out, double *absmag);
 int oracle_residual_f32(const float *const *F, int n, const double *w,
                         const int64_t *slot_offset, const int64_t *seg_numel,
                         const int64_t *res_offset, int n_segs, const double *x_in,

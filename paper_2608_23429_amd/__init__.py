@@ -13,7 +13,7 @@ import numpy as np
 import torch
 
 from ._binding import (  # noqa: F401  (re-exported C entry points)
-    CHEB_BF16, CHEB_F32, CHEB_MAX_NODES, CHEB_MAX_OUTPUTS, CHEB_MAX_SLOTS, CHEB_RHO_ALTERNATING,
+    CHEB_BF16, CHEB_F16, CHEB_F32, CHEB_MAX_NODES, CHEB_MAX_OUTPUTS, CHEB_MAX_SLOTS, CHEB_RHO_ALTERNATING,
     CHEB_RHO_GENERAL, CHEB_SHORT_FULL, CHEB_TAYLOR, CHEB_SHORT_LOWER, ChebError, cheb_chebyshev_nodes,
     cheb_precompute_weights_variant,
     cheb_cache_abort_push, cheb_cache_begin_push, cheb_cache_commit, cheb_cache_create,
@@ -31,8 +31,8 @@ from . import _binding
 
 LIB_PATH = _binding.LIB_PATH
 
-_DTYPES = {torch.bfloat16: CHEB_BF16, torch.float32: CHEB_F32}
-_TORCH = {CHEB_BF16: torch.bfloat16, CHEB_F32: torch.float32}
+_DTYPES = {torch.bfloat16: CHEB_BF16, torch.float16: CHEB_F16, torch.float32: CHEB_F32}
+_TORCH = {CHEB_BF16: torch.bfloat16, CHEB_F16: torch.float16, CHEB_F32: torch.float32}
 
 
 def cheb_dtype(dtype: torch.dtype) -> int:

@@ -32,6 +32,7 @@ CHEB_TAYLOR = 2
 
 CHEB_BF16 = 0
 CHEB_F32 = 1
+CHEB_F16 = 2
 CHEB_MAX_SLOTS = 8
 CHEB_MAX_OUTPUTS = 8
 CHEB_MAX_NODES = 64

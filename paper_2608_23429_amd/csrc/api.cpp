@@ -343,8 +343,8 @@ int cheb_combine_multi(const void *const *src, int32_t n_src, const double *w, i
     return fail(CHEB_E_INVAL, "numel %lld too large for one launch", (long long)numel);
   for (int m = 0; m < n_out * n_src; ++m) {
     if (!isfinite(w[m])) return fail(CHEB_E_NONFINITE, "weight %d is not finite", m);
-    // The bf16 kernel takes its weights as fp32.
-    if (dtype == CHEB_BF16 && fabs(w[m]) > double(FLT_MAX))
+    // The bf16 and fp16 kernels take their weights as fp32.
+    if (dtype != CHEB_F32 && fabs(w[m]) > double(FLT_MAX))
       return fail(CHEB_E_NONFINITE, "weight %d (%.17g) overflows fp32", m, w[m]);
   }
   if (numel == 0) return ok();

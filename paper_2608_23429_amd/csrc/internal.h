@@ -17,9 +17,11 @@ int fail(int code, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
 int ok();
 
 // Storage type traits.
-inline int elem_bytes(int dtype) { return dtype == CHEB_BF16 ? 2 : 4; }
+inline int elem_bytes(int dtype) { return dtype == CHEB_F32 ? 4 : 2; }
 inline int elems_per_vec(int dtype) { return 16 / elem_bytes(dtype); }
-inline bool valid_dtype(int dtype) { return dtype == CHEB_BF16 || dtype == CHEB_F32; }
+inline bool valid_dtype(int dtype) {
+  return dtype == CHEB_BF16 || dtype == CHEB_F32 || dtype == CHEB_F16;
+}
 
 // Largest number of 16-byte vectors one streaming launch covers (keeps every
 // in-kernel index below 2^31 so 32-bit index arithmetic cannot wrap).

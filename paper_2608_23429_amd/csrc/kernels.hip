@@ -9,9 +9,10 @@
 //    for bandwidth: 128-bit coalesced loads (a wave covers 1 KiB contiguous
 //    per load instruction), all n x unroll loads of a thread issued before
 //    any arithmetic, weights as kernel arguments (they live in SGPRs), fp32
-//    accumulation for bf16 storage and fp64 for fp32 storage, and one
-//    hardware round-to-nearest-even pack per element pair
-//    (v_cvt_pk_bf16_f32).  No LDS: nothing is reused across lanes.
+//    accumulation for bf16 and fp16 storage and fp64 for fp32 storage, and
+//    one hardware round-to-nearest-even pack per element pair
+//    (v_cvt_pk_bf16_f32, v_cvt_pk_f16_f32).  No LDS: nothing is reused
+//    across lanes.
 // 2. The full-step push (Algorithm 1, full computation: store (s, f_s) in
 //    the history): one launch copies up to 64 segments into a slot.
 // 3. Residual application on a skipped step (Section 3.1, block equation):
@@ -32,6 +33,7 @@ namespace {
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 
 template <bool NT>
 __device__ __forceinline__ u32x4 load16(const u32x4 *p) {
@@ -106,6 +108,53 @@ struct Bf16Op {
 #pragma unroll
     for (int k = 1; k < NS; ++k) a = fmaf(w[k], __uint_as_float(uint32_t(p[k][i]) << 16), a);
     return __builtin_bit_cast(uint16_t, static_cast<__bf16>(a));
+  }
+};
+
+// ---- binary16 storage, fp32 accumulation ---------------------------------
+
+struct F16Op {
+  using W = float;
+  using E = uint16_t;
+
+  __device__ __forceinline__ static f32x2 pair(uint32_t word) {  // elements 2q, 2q+1
+    return __builtin_convertvector(__builtin_bit_cast(f16x2, word), f32x2);
+  }
+
+  template <int NS>
+  __device__ __forceinline__ static u32x4 vec(const u32x4 (&v)[NS], const W (&w)[NS]) {
+    float a[8];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const f32x2 p = pair(v[0][q]);
+      a[2 * q] = w[0] * p.x;
+      a[2 * q + 1] = w[0] * p.y;
+    }
+#pragma unroll
+    for (int k = 1; k < NS; ++k) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const f32x2 p = pair(v[k][q]);
+        a[2 * q] = fmaf(w[k], p.x, a[2 * q]);
+        a[2 * q + 1] = fmaf(w[k], p.y, a[2 * q + 1]);
+      }
+    }
+    u32x4 r;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      f32x2 pr = {a[2 * q], a[2 * q + 1]};
+      r[q] = __builtin_bit_cast(uint32_t, __builtin_convertvector(pr, f16x2));
+    }
+    return r;
+  }
+
+  template <int NS>
+  __device__ __forceinline__ static E scalar(const E *const (&p)[NS], const W (&w)[NS],
+                                             uint64_t i) {
+    float a = w[0] * float(__builtin_bit_cast(_Float16, p[0][i]));
+#pragma unroll
+    for (int k = 1; k < NS; ++k) a = fmaf(w[k], float(__builtin_bit_cast(_Float16, p[k][i])), a);
+    return __builtin_bit_cast(uint16_t, static_cast<_Float16>(a));
   }
 };
 
@@ -356,6 +405,18 @@ struct Bf16Dec {
   }
 };
 
+struct F16Dec {
+  static constexpr int kVec = 8;
+  __device__ __forceinline__ static void add(double (&a)[8], u32x4 v, double w) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const f32x2 p = F16Op::pair(v[q]);
+      a[2 * q] = fma(w, double(p.x), a[2 * q]);
+      a[2 * q + 1] = fma(w, double(p.y), a[2 * q + 1]);
+    }
+  }
+};
+
 struct F32Dec {
   static constexpr int kVec = 4;
   __device__ __forceinline__ static void add(double (&a)[4], u32x4 v, double w) {
@@ -491,9 +552,12 @@ int launch_combine(int dtype, const void *const *src, int n, const double *w, in
   int rc = device_cus(&cus);
   if (rc != CHEB_OK) return rc;
   const cheb_launch_config cfg = launch_shape();
-  hipError_t e = dtype == CHEB_BF16
-                     ? launch_op<Bf16Op>(src, n, w, n_out, out, numel, cfg, cus, stream)
-                     : launch_op<F32Op>(src, n, w, n_out, out, numel, cfg, cus, stream);
+  hipError_t e;
+  switch (dtype) {
+    case CHEB_BF16: e = launch_op<Bf16Op>(src, n, w, n_out, out, numel, cfg, cus, stream); break;
+    case CHEB_F16: e = launch_op<F16Op>(src, n, w, n_out, out, numel, cfg, cus, stream); break;
+    default: e = launch_op<F32Op>(src, n, w, n_out, out, numel, cfg, cus, stream); break;
+  }
   if (e != hipSuccess) return fail(CHEB_E_HIP, "combine launch failed: %s", hipGetErrorString(e));
   return ok();
 }
@@ -522,7 +586,7 @@ int launch_gather(int dtype, void *slot_base, const GatherSeg *segs, int n_segs,
     a.n = used;
     char *slot = static_cast<char *>(slot_base);
     const dim3 grid{static_cast<uint32_t>(max_chunks), static_cast<uint32_t>(used), 1u};
-    if (dtype == CHEB_BF16)
+    if (elem_bytes(dtype) == 2)
       hipLaunchKernelGGL(gather_kernel<uint16_t>, grid, dim3(kGatherBlock), 0, stream, a, slot);
     else
       hipLaunchKernelGGL(gather_kernel<float>, grid, dim3(kGatherBlock), 0, stream, a, slot);
@@ -542,11 +606,19 @@ int launch_residual(int dtype, int n, const uint64_t *base, const double *w, con
                     int ncover, const float *x_in, float *x_out, int64_t vec_begin,
                     int64_t n_vec, hipStream_t stream) {
   if (n_vec == 0) return ok();
-  hipError_t e = dtype == CHEB_BF16
-                     ? launch_residual_dec<Bf16Dec>(n, base, w, delta, ncover, x_in, x_out,
-                                                    uint32_t(vec_begin), uint32_t(n_vec), stream)
-                     : launch_residual_dec<F32Dec>(n, base, w, delta, ncover, x_in, x_out,
-                                                   uint32_t(vec_begin), uint32_t(n_vec), stream);
+  const uint32_t vb = uint32_t(vec_begin), nv = uint32_t(n_vec);
+  hipError_t e;
+  switch (dtype) {
+    case CHEB_BF16:
+      e = launch_residual_dec<Bf16Dec>(n, base, w, delta, ncover, x_in, x_out, vb, nv, stream);
+      break;
+    case CHEB_F16:
+      e = launch_residual_dec<F16Dec>(n, base, w, delta, ncover, x_in, x_out, vb, nv, stream);
+      break;
+    default:
+      e = launch_residual_dec<F32Dec>(n, base, w, delta, ncover, x_in, x_out, vb, nv, stream);
+      break;
+  }
   if (e != hipSuccess) return fail(CHEB_E_HIP, "residual launch failed: %s", hipGetErrorString(e));
   return ok();
 }

@@ -21,7 +21,7 @@ import math
 class Config:
     name: str
     index: int
-    dtype: str                      # "bf16" or "f32": storage type of the cache
+    dtype: str                      # "bf16", "f16" or "f32": storage type of the cache
     segments: Tuple[Tuple[int, ...], ...]   # cached tensor shapes, in cache order
     segment_names: Tuple[str, ...]
     nodes: Tuple[float, ...]        # history abscissae, oldest to newest
@@ -48,7 +48,7 @@ class Config:
 
     @property
     def elem_size(self) -> int:
-        return 2 if self.dtype == "bf16" else 4
+        return 4 if self.dtype == "f32" else 2
 
     @property
     def seg_numel(self) -> List[int]:

@@ -21,7 +21,7 @@ import torch
 
 from .configs import Config
 
-_TORCH_DTYPES = {"bf16": torch.bfloat16, "f32": torch.float32}
+_TORCH_DTYPES = {"bf16": torch.bfloat16, "f16": torch.float16, "f32": torch.float32}
 
 
 def torch_dtype(cfg: Config) -> torch.dtype:

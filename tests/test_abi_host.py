@@ -179,7 +179,7 @@ def _expected_layout(n_slots, esize, seg):
     return off, pos, stride, stride * n_slots
 
 
-@pytest.mark.parametrize("dtype,esize", [(B.CHEB_BF16, 2), (B.CHEB_F32, 4)])
+@pytest.mark.parametrize("dtype,esize", [(B.CHEB_BF16, 2), (B.CHEB_F16, 2), (B.CHEB_F32, 4)])
 def test_layout_rounding(dtype, esize):
     seg = [1, 8, 13, 0, 1000003, 3, 4096 * 3072]
     lay = cheb.cheb_cache_layout(5, dtype, seg)

@@ -8,7 +8,7 @@ import torch
 import oracle
 import paper_2608_23429_amd as cheb
 from synth import CONFIGS, make_history, split_segments, by_name
-from tests.gpu_util import check_parity, say, to_host_bits
+from tests.gpu_util import TOL, check_parity, decode, oracle_combine, say, to_host_bits
 
 pytestmark = pytest.mark.gpu
 
@@ -17,11 +17,11 @@ def _classes(v):
     return np.where(np.isnan(v), 0, np.where(np.isposinf(v), 1, np.where(np.isneginf(v), 2, 3)))
 
 
-@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("dtype", ["bf16", "f16", "f32"])
 def test_nonfinite_inputs_propagate_like_ieee(dtype):
     """NaN and +-Inf planted in the history: the output is NaN / +-Inf
     exactly where the fp64 oracle's is, finite elements keep the bound."""
-    td = torch.bfloat16 if dtype == "bf16" else torch.float32
+    td = {"bf16": torch.bfloat16, "f16": torch.float16, "f32": torch.float32}[dtype]
     n, numel = 5, 100_003
     g = torch.Generator(device="cuda")
     g.manual_seed(19)
@@ -36,13 +36,13 @@ def test_nonfinite_inputs_propagate_like_ieee(dtype):
     cheb.combine(srcs, w, out)
     torch.cuda.synchronize()
     hosts = [to_host_bits(s) for s in srcs]
-    exp, mag = (oracle.extrapolate_bf16 if dtype == "bf16" else oracle.extrapolate_f32)(hosts, w)
-    got = oracle.bf16_to_f64(to_host_bits(out)) if dtype == "bf16" else to_host_bits(out).astype(np.float64)
+    exp, mag = oracle_combine(hosts, w, dtype)
+    got = decode(to_host_bits(out), dtype)
     fin = np.isfinite(exp)
     assert (~fin).sum() > 1000
     assert np.array_equal(_classes(got[~fin]), _classes(exp[~fin]))
     e = oracle.parity_error(got[fin], exp[fin], mag[fin])[0]
-    assert e <= (1e-2 if dtype == "bf16" else 1e-5)
+    assert e <= TOL[dtype]
 
 
 def test_target_on_a_held_node_is_a_bit_copy():
@@ -109,25 +109,25 @@ def test_push_then_predict_ordered_on_one_stream():
 def _max_numel(dtype):
     """Largest element count one launch takes: 2^31 - 1 whole 16-byte
     vectors plus a ragged tail of one element less than a vector."""
-    per_vec = 8 if dtype == "bf16" else 4
+    per_vec = 4 if dtype == "f32" else 8
     return ((1 << 31) - 1) * per_vec + per_vec - 1
 
 
-@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("dtype", ["bf16", "f16", "f32"])
 def test_largest_launch(dtype):
     """The largest problem the host accepts in one launch (32 GiB per
     buffer; the kernel's 32-bit vector indices reach 2^31 - 1): two sources,
     then two outputs from one pass, sampled against the oracle at both ends,
     around the last tile and at random."""
     numel = _max_numel(dtype)
-    nbytes = numel * (2 if dtype == "bf16" else 4)
+    nbytes = numel * (4 if dtype == "f32" else 2)
     torch.cuda.synchronize()
     torch.cuda.empty_cache()                        # blocks cached by earlier tests
     free, _ = torch.cuda.mem_get_info()
     if free < 4 * nbytes + (8 << 30):
         pytest.skip(f"needs {4 * nbytes + (8 << 30)} free bytes, {free} free")
     say(f"largest launch {dtype}: {numel} elements, {nbytes} bytes per buffer")
-    td = torch.bfloat16 if dtype == "bf16" else torch.float32
+    td = {"bf16": torch.bfloat16, "f16": torch.float16, "f32": torch.float32}[dtype]
     g = torch.Generator(device="cuda")
     g.manual_seed(31)
     srcs = [torch.empty(numel, dtype=td, device="cuda").uniform_(-1.0, 1.0, generator=g)

@@ -12,7 +12,7 @@ from tests.gpu_util import check_parity, say, to_host_bits
 
 pytestmark = pytest.mark.gpu
 
-DT = {"bf16": torch.bfloat16, "f32": torch.float32}
+DT = {"bf16": torch.bfloat16, "f16": torch.float16, "f32": torch.float32}
 
 
 def _rand(n, numel, dtype, seed):
@@ -21,7 +21,7 @@ def _rand(n, numel, dtype, seed):
     return [torch.randn(numel, generator=g, device="cuda").to(DT[dtype]) for _ in range(n)]
 
 
-@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("dtype", ["bf16", "f16", "f32"])
 @pytest.mark.parametrize("n_src", [1, 3, 6, 8])
 def test_combine_multi_all_output_counts(dtype, n_src):
     rng = np.random.default_rng(n_src)
@@ -42,8 +42,8 @@ def test_combine_multi_all_output_counts(dtype, n_src):
                 single = torch.empty_like(outs[m])
                 cheb.combine(srcs, w[m], single)
                 torch.cuda.synchronize()
-                assert torch.equal(single.view(torch.int16 if dtype == "bf16" else torch.int32),
-                                   outs[m].view(torch.int16 if dtype == "bf16" else torch.int32))
+                assert torch.equal(single.view(torch.int32 if dtype == "f32" else torch.int16),
+                                   outs[m].view(torch.int32 if dtype == "f32" else torch.int16))
 
 
 @pytest.mark.parametrize("cfg", CONFIGS, ids=lambda c: c.name)

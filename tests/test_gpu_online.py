@@ -14,7 +14,7 @@ from tests.gpu_util import check_parity, say, to_host_bits
 
 pytestmark = pytest.mark.gpu
 
-DT = {"bf16": torch.bfloat16, "f32": torch.float32}
+DT = {"bf16": torch.bfloat16, "f16": torch.float16, "f32": torch.float32}
 
 # (workload, T, s0, s1, r, n, policy, abscissa of step s)
 CASES = [

@@ -5,6 +5,8 @@ copies of the same stored values.  Floating-point results must satisfy the
 floored relative bound (1e-2 for bfloat16 storage, 1e-5 for float32 storage);
 bit patterns are compared exactly where the result is fixed bit for bit.
 """
+from dataclasses import replace
+
 import numpy as np
 import pytest
 import torch
@@ -16,7 +18,7 @@ from tests.gpu_util import TOL, check_parity, decode, say, to_host_bits
 
 pytestmark = pytest.mark.gpu
 
-DT = {"bf16": torch.bfloat16, "f32": torch.float32}
+DT = {"bf16": torch.bfloat16, "f16": torch.float16, "f32": torch.float32}
 SHAPES = [
     {"block": 1024, "unroll": 1, "nontemporal": 1, "blocks_per_cu": 0},
     {"block": 256, "unroll": 4, "nontemporal": 1, "blocks_per_cu": 0},
@@ -51,7 +53,7 @@ def _rand(n, numel, dtype, seed, scale=1.0):
 NUMELS = [1, 7, 8, 9, 255, 1000, 65536 + 13, 3 * 4 * 256 * 8 + 5, 1 << 20]
 
 
-@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("dtype", ["bf16", "f16", "f32"])
 @pytest.mark.parametrize("n", range(1, 9))
 def test_combine_all_sizes(dtype, n):
     rng = np.random.default_rng(1000 + n)
@@ -68,7 +70,7 @@ def test_combine_all_sizes(dtype, n):
 
 
 @pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "b{block}_u{unroll}_nt{nontemporal}_g{blocks_per_cu}".format(**s))
-@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("dtype", ["bf16", "f16", "f32"])
 def test_combine_launch_shapes(shape, dtype):
     cheb.cheb_set_launch_config(**shape)
     n = 6
@@ -99,7 +101,7 @@ def test_combine_empty_and_nonzero_stream():
 # Bit-exact special cases
 # --------------------------------------------------------------------------
 
-@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("dtype", ["bf16", "f16", "f32"])
 def test_unit_weights_copy_bitwise(dtype):
     """w = e_j: every output is entry j's stored value (K = 0 is the n = 1 case)."""
     numel = 123_457
@@ -139,6 +141,42 @@ def test_bf16_midpoint_weights_round_to_nearest_even():
     assert ties.any()
 
 
+def test_f16_midpoint_weights_round_to_nearest_even():
+    """w = (1/2, 1/2) on float16 inputs in [1, 2): the fp32 sum is exact, so
+    the output must be the correctly rounded float16 of the exact mean (the
+    oracle's binary16 rounding), ties included."""
+    numel = 1 << 18
+    g = torch.Generator(device="cuda")
+    g.manual_seed(5)
+    a = (torch.rand(numel, generator=g, device="cuda") + 1.0).to(torch.float16)
+    b = (torch.rand(numel, generator=g, device="cuda") + 1.0).to(torch.float16)
+    out = torch.empty(numel, dtype=torch.float16, device="cuda")
+    cheb.combine([a, b], [0.5, 0.5], out)
+    torch.cuda.synchronize()
+    exact = 0.5 * oracle.f16_to_f64(to_host_bits(a)) + 0.5 * oracle.f16_to_f64(to_host_bits(b))
+    assert np.array_equal(to_host_bits(out), oracle.round_f16(exact))
+    ties = np.mod(exact * 2048.0, 2.0) == 1.0    # inputs are multiples of 2^-10
+    assert ties.any()
+
+
+def test_f16_overflow_and_subnormal_outputs():
+    """float16 results past the largest finite value become +-Inf, and tiny
+    results land on the subnormals, exactly as the oracle's rounding of the
+    fp32 sum (weights (1, 1) keep every sum exact in fp32)."""
+    numel = 1 << 16
+    g = torch.Generator(device="cuda")
+    g.manual_seed(6)
+    big = ((torch.rand(numel, generator=g, device="cuda") * 2 - 1) * 60000.0).to(torch.float16)
+    tiny = ((torch.rand(numel, generator=g, device="cuda") * 2 - 1) * 6e-5).to(torch.float16)
+    for x in (big, tiny):
+        out = torch.empty_like(x)
+        cheb.combine([x, x], [1.0, 1.0], out)
+        torch.cuda.synchronize()
+        exact = 2.0 * oracle.f16_to_f64(to_host_bits(x))
+        assert np.array_equal(to_host_bits(out), oracle.round_f16(exact))
+    assert np.isinf(oracle.f16_to_f64(oracle.round_f16(2.0 * oracle.f16_to_f64(to_host_bits(big))))).any()
+
+
 # --------------------------------------------------------------------------
 # History ring on the device
 # --------------------------------------------------------------------------
@@ -146,7 +184,7 @@ def test_bf16_midpoint_weights_round_to_nearest_even():
 RAGGED = [13, 1, 8, 1_000_003, 0, 4096 * 3 + 7]
 
 
-@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("dtype", ["bf16", "f16", "f32"])
 def test_ring_push_eviction_and_padding(dtype):
     n = 4
     cache = cheb.ChebCache(n, DT[dtype], RAGGED)
@@ -169,7 +207,8 @@ def test_ring_push_eviction_and_padding(dtype):
             for s, (off, m) in enumerate(zip(cache.seg_offset, cache.seg_numel)):
                 assert np.array_equal(flat[off:off + m], to_host_bits(psegs[s])), (i, age, s)
                 end = off + m
-                pad_end = -(-m // (8 if dtype == "bf16" else 4)) * (8 if dtype == "bf16" else 4) + off
+                vec = 4 if dtype == "f32" else 8
+                pad_end = -(-m // vec) * vec + off
                 assert np.all(flat[end:pad_end] == 0), "padding not zeroed"
     # Prediction over the held entries, per segment, against the oracle.
     out, w = cache.extrapolate_at(859.0)
@@ -183,7 +222,7 @@ def test_ring_push_eviction_and_padding(dtype):
     cache.close()
 
 
-@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("dtype", ["bf16", "f16", "f32"])
 def test_fused_push_matches_copy_push(dtype):
     seg = [4096 * 8, 1000, 24]
     a = cheb.ChebCache(3, DT[dtype], seg)
@@ -207,8 +246,8 @@ def test_fused_push_matches_copy_push(dtype):
         check_parity(to_host_bits(va), [to_host_bits(p[s_idx]) for p in pushed[1:]], w, dtype,
                      f"copy push segment {s_idx}")
     for va, vb in zip(a.segment_views(oa), b.segment_views(ob)):
-        assert torch.equal(va.view(torch.int16 if dtype == "bf16" else torch.int32),
-                           vb.view(torch.int16 if dtype == "bf16" else torch.int32))
+        assert torch.equal(va.view(torch.int32 if dtype == "f32" else torch.int16),
+                           vb.view(torch.int32 if dtype == "f32" else torch.int16))
     a.close()
     b.close()
 
@@ -233,7 +272,13 @@ def _run_workload(cfg, nodes, targets, time_scale=None, label=""):
     return cache, entries, outs, ws
 
 
-@pytest.mark.parametrize("cfg", CONFIGS, ids=lambda c: c.name)
+# The paper's PixArt-Sigma and DiT-XL/2 also run with float16 activations:
+# the same workloads with float16 storage.
+F16_WORKLOADS = [replace(by_name("pixart_sigma_1024"), name="pixart_sigma_1024_f16", dtype="f16"),
+                 replace(by_name("dit_xl2_256"), name="dit_xl2_256_f16", dtype="f16")]
+
+
+@pytest.mark.parametrize("cfg", CONFIGS + F16_WORKLOADS, ids=lambda c: c.name)
 def test_workload_small_all_elements(cfg):
     """Each workload's schedule and generator on a cache cut down so the
     oracle checks every element (ragged segment mix kept)."""
@@ -265,7 +310,7 @@ def _sample_indices(numel, seg_offsets, seg_numel, count, seed):
     return np.unique(np.concatenate(idx))
 
 
-@pytest.mark.parametrize("cfg", CONFIGS, ids=lambda c: c.name)
+@pytest.mark.parametrize("cfg", CONFIGS + F16_WORKLOADS, ids=lambda c: c.name)
 def test_workload_full_size_sampled(cfg):
     """Full cache shape, default launch shape (the one the benchmark times):
     the oracle recomputes a sample of outputs (random elements, both ends of

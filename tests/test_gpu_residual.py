@@ -1,6 +1,8 @@
 """Residual application on a skipped step (block equation of Section 3.1
 with every module output predicted) and the collapsed history, through the
 C ABI, against the oracle's plain per-segment fp64 definition."""
+from dataclasses import replace
+
 import numpy as np
 import pytest
 import torch
@@ -12,7 +14,7 @@ from tests.gpu_util import say, to_host_bits
 
 pytestmark = pytest.mark.gpu
 
-DT = {"bf16": torch.bfloat16, "f32": torch.float32}
+DT = {"bf16": torch.bfloat16, "f16": torch.float16, "f32": torch.float32}
 RES_TOL = 1e-5      # fp64 accumulation, one fp32 rounding of the result
 COLLAPSED_TOL = 1e-2  # bfloat16-storage bound; entries rounded once to fp32
 
@@ -43,6 +45,7 @@ SMALL = [
     ("pixart", lambda: by_name("pixart_sigma_1024").scaled_blocks(64, 3)),
     ("flux", lambda: by_name("flux_dev_1024").scaled_blocks(32, 3)),
     ("tiny", lambda: by_name("tiny")),
+    ("pixart_f16", lambda: replace(by_name("pixart_sigma_1024").scaled_blocks(64, 3), dtype="f16")),
 ]
 
 

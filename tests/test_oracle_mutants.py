@@ -58,6 +58,13 @@ MUTANTS = [
      "((j == 0) ? 0.5 : 1.0)", 0),
     ("alternating weights without sign", "double rho = ((j % 2) ? -1.0 : 1.0)", "double rho = ((j % 2) ? 1.0 : 1.0)", 0),
     ("Chebyshev roots shifted", "cos((2.0 * j - 1.0) * pi / (2.0 * n))", "cos((2.0 * j) * pi / (2.0 * n))", 0),
+    ("f16 exponent bias", "v = ldexp((double)(1024 + frac), expo - 25);",
+     "v = ldexp((double)(1024 + frac), expo - 24);", 0),
+    ("f16 subnormal scale", "v = ldexp((double)frac, -24);", "v = ldexp((double)frac, -25);", 0),
+    ("f16 ties away from zero", "if (frac > 0.5 || (frac == 0.5 && fmod(r, 2.0) != 0.0)) r += 1.0;\n  const double rounded",
+     "if (frac >= 0.5) r += 1.0;\n  const double rounded", 0),
+    ("f16 overflow loses the sign", "if (rounded >= 65536.0) return (uint16_t)(sign | 0x7C00);",
+     "if (rounded >= 65536.0) return (uint16_t)0x7C00;", 0),
     ("Taylor about the oldest node", "const double d = xstar - x[n - 1];", "const double d = xstar - x[0];", 0),
     ("Taylor divided difference over adjacent nodes only",
      "(table[k] - table[k - 1]) / (x[k] - x[k - i])", "(table[k] - table[k - 1]) / (x[k] - x[k - 1])", 0),

@@ -328,6 +328,75 @@ def test_round_bf16_agrees_with_torch_on_f32_inputs():
     assert np.array_equal(mine, ref)
 
 
+def test_f16_decode_all_patterns_matches_numpy():
+    bits = np.arange(65536, dtype=np.uint16)
+    mine = oracle.f16_to_f64(bits)
+    ref = bits.view(np.float16).astype(np.float64)
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(mine), nan)
+    assert np.array_equal(mine[~nan], ref[~nan])
+    assert np.array_equal(np.signbit(mine[~nan]), np.signbit(ref[~nan]))
+    # spot values from the format's definition
+    assert oracle.f16_to_f64([0x3C00, 0x7BFF, 0x0001, 0x0400, 0xC000]).tolist() == \
+        [1.0, 65504.0, 2.0 ** -24, 2.0 ** -14, -2.0]
+
+
+def _decode16(b):
+    return oracle.f16_to_f64(np.array([b], dtype=np.uint16))[0]
+
+
+def test_round_f16_is_nearest_ties_to_even():
+    """Brute force over neighbours: the chosen pattern is the nearest finite
+    binary16 value, and on an exact tie it has an even last significand bit;
+    values from 65520 up (the largest finite plus half its spacing) become
+    infinity."""
+    rng = np.random.default_rng(37)
+    exps = rng.integers(-27, 17, size=3000)
+    v = rng.uniform(1.0, 2.0, size=3000) * np.ldexp(1.0, exps) * rng.choice([-1, 1], 3000)
+    ties = np.array([_decode16(b) for b in list(range(0x3C00, 0x3C10)) + list(range(0x0001, 0x0011))])
+    mids = np.concatenate([(ties[:15] + ties[1:16]) / 2, (ties[16:-1] + ties[17:]) / 2])
+    v = np.concatenate([v, mids, -mids, [0.0, -0.0, 1e-12, 65504.0, 65519.99, 65520.0, 7e4]])
+    got = oracle.round_f16(v)
+    for x, b in zip(v, got):
+        b = int(b)
+        d = _decode16(b)
+        if math.isinf(d):
+            assert abs(x) >= 65520.0
+            continue
+        cand = [c for c in ((b - 1) & 0xFFFF, (b + 1) & 0xFFFF) if (c & 0x7C00) != 0x7C00]
+        for c in cand:
+            dc = _decode16(c)
+            assert abs(x - d) <= abs(x - dc), (x, hex(b), hex(c))
+            if abs(x - d) == abs(x - dc) and dc != d:
+                assert b % 2 == 0, (x, hex(b))
+    for lo in list(range(0x3C00, 0x3C0F)) + list(range(0x0001, 0x0010)):
+        m = (_decode16(lo) + _decode16(lo + 1)) / 2
+        assert int(oracle.round_f16([m])[0]) == (lo if lo % 2 == 0 else lo + 1), hex(lo)
+
+
+def test_round_f16_agrees_with_numpy():
+    """numpy's float64 -> float16 conversion rounds to nearest even."""
+    rng = np.random.default_rng(41)
+    v = rng.standard_normal(200000) * np.exp(rng.uniform(-20, 12, 200000))
+    with np.errstate(over="ignore"):
+        ref = v.astype(np.float16).view(np.uint16)
+    assert np.array_equal(oracle.round_f16(v), ref)
+
+
+def test_extrapolate_f16_decodes_exactly():
+    rng = np.random.default_rng(43)
+    vals = (rng.standard_normal((5, 2001)) * 3).astype(np.float16)
+    bits = [v.view(np.uint16) for v in vals]
+    w = oracle.weights_row([4, 8, 12, 16, 20], 21)
+    out, mag = oracle.extrapolate_f16(bits, w)
+    dec = vals.astype(np.float64)
+    ref = np.zeros(vals.shape[1])
+    for k in range(5):            # written out: oldest to newest, fp64
+        ref = ref + w[k] * dec[k]
+    np.testing.assert_array_equal(out, ref)
+    np.testing.assert_allclose(mag, np.abs(w) @ np.abs(dec), rtol=1e-15)
+
+
 # --------------------------------------------------------------------------
 # Schedule
 # --------------------------------------------------------------------------
