@@ -94,7 +94,7 @@ def copy_probe(torch):
 def setup_workload(torch, cheb, cfg):
     """Seeded history on the device, pushed through the ring."""
     from synth import make_history, split_segments
-    dt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    dt = {"bf16": torch.bfloat16, "f16": torch.float16, "f32": torch.float32}[cfg.dtype]
     t0 = time.time()
     entries = make_history(cfg, "cuda")
     torch.cuda.synchronize()
@@ -258,7 +258,7 @@ def time_online_run(torch, cheb, cfg, entries, reps=3):
     table = cheb.ChebTable(T, s0, s1, r, n, x, cheb.CHEB_SHORT_FULL)
     predicted = [table.step(s)[0] for s in range(T)]
     runs = dict(table.runs())
-    dt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    dt = {"bf16": torch.bfloat16, "f16": torch.float16, "f32": torch.float32}[cfg.dtype]
     cache = cheb.ChebCache(n, dt, cfg.seg_numel)
     outs = [cache.new_output() for _ in range(max(runs.values()))]
     segs = [split_segments(e, cfg) for e in entries]
@@ -435,7 +435,7 @@ def time_rotated(torch, cheb, cfg, entries, sets=32, steps=64):
     with its own output, so that the working set (sets x (K+2) entries) is
     larger than the 256 MB last-level cache and every step streams from HBM."""
     from synth import split_segments
-    dt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    dt = {"bf16": torch.bfloat16, "f16": torch.float16, "f32": torch.float32}[cfg.dtype]
     pairs = []
     for _ in range(sets):
         c = cheb.ChebCache(cfg.n_hist, dt, cfg.seg_numel)
@@ -536,7 +536,7 @@ def main(argv=None):
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16" if cfg.dtype == "bf16" else "f32",
+        "dtype": cfg.dtype,
         "data": "synthetic: seeded per-element random polynomial in the time variable plus "
                 "Gaussian noise, stored in the cache dtype",
         "config": {"workload": cfg.name, "elements_per_entry": cfg.numel,
@@ -565,9 +565,11 @@ def main(argv=None):
     del entries, cache, out
     torch.cuda.empty_cache()
     if args.other_configs:
+        from dataclasses import replace
         from synth import CONFIGS
         per = []
-        for c in CONFIGS:
+        f16 = replace(by_name("pixart_sigma_1024"), name="pixart_sigma_1024_f16", dtype="f16")
+        for c in CONFIGS + [f16]:
             if c.name == cfg.name:
                 continue
             r, e, ch, o = measure_config(torch, cheb, c, max(10, args.steps // 2), args.warmup)
