@@ -115,7 +115,7 @@ def test_residual_partial_coverage_and_unmapped_segments():
     cache.close()
 
 
-@pytest.mark.parametrize("case", SMALL[:3], ids=lambda c: c[0])
+@pytest.mark.parametrize("case", SMALL[:3] + SMALL[4:], ids=lambda c: c[0])
 def test_collapsed_history_equals_full_form(case):
     """Push-time reduction into a residual-sized fp32 ring, then the skipped
     step's residual from it, against the oracle on the full history."""
@@ -130,7 +130,7 @@ def test_collapsed_history_equals_full_form(case):
     seg_off = [int(o) for o in lay["seg_offset"]]
     red = hist.cache.entry(cfg.n_hist - 1)[:res_n].cpu().numpy()
     exp1, mag1 = oracle.residual([to_host_bits(entries[-1])], [1.0], seg_off, cfg.seg_numel,
-                                 res_off, res_n)
+                                 res_off, res_n, dtype=cfg.dtype)
     _check(red, exp1, mag1, RES_TOL, "push-time reduction")
     x_in = _x_in(res_n, 11)
     for t in cfg.targets:
@@ -139,7 +139,7 @@ def test_collapsed_history_equals_full_form(case):
         torch.cuda.synchronize()
         exp, mag = oracle.residual([to_host_bits(e) for e in entries],
                                    oracle.weights_row(cfg.nodes, t), seg_off, cfg.seg_numel,
-                                   res_off, res_n, x_in=x_in.cpu().numpy())
+                                   res_off, res_n, x_in=x_in.cpu().numpy(), dtype=cfg.dtype)
         _check(x_out.cpu().numpy(), exp, mag, COLLAPSED_TOL, f"collapsed t={t}")
     hist.close()
 
