@@ -28,9 +28,10 @@
  *     stream.  GPU work is asynchronous on that stream.  Calls enqueue work in
  *     program order; the caller orders work across streams.
  *   - History order is always oldest to newest.
- *   - Storage types: CHEB_BF16 (bfloat16) storage with fp32 accumulation and
- *     round-to-nearest-even output; CHEB_F32 (binary32) storage with fp64
- *     accumulation and round-to-nearest-even output.
+ *   - Storage types: CHEB_BF16 (bfloat16) and CHEB_F16 (binary16) storage
+ *     with fp32 weights and accumulation and round-to-nearest-even output;
+ *     CHEB_F32 (binary32) storage with fp64 weights and accumulation and
+ *     round-to-nearest-even output.
  *   - Distinct cache handles may be used from different threads at once.  One
  *     handle must not be used by two threads at the same time.
  */
@@ -44,7 +45,7 @@
 extern "C" {
 #endif
 
-#define CHEB_VERSION 1
+#define CHEB_VERSION 2
 
 #if defined(__GNUC__) || defined(__clang__)
 #define CHEB_API __attribute__((visibility("default")))

@@ -45,7 +45,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_version():
-    assert cheb.cheb_version() == 1
+    assert cheb.cheb_version() == 2
 
 
 def _wtol(w, factor=8.0):
