@@ -16,7 +16,13 @@ pytestmark = pytest.mark.gpu
 
 DT = {"bf16": torch.bfloat16, "f16": torch.float16, "f32": torch.float32}
 RES_TOL = 1e-5      # fp64 accumulation, one fp32 rounding of the result
-COLLAPSED_TOL = 1e-2  # bfloat16-storage bound; entries rounded once to fp32
+# Collapsed history: each entry r_k is the fp64 sum of one full step's module
+# outputs rounded once to fp32, so |r_k - exact_k| <= 2^-24 |exact_k| <=
+# 2^-24 sum_s |F_k[s]|; the prediction adds sum_k |w_k| of that, at most
+# 2^-24 times the oracle's magnitude S, and rounds the fp64 result once to
+# fp32 (2^-24 |o|).  Against max(|o|, 10^-3 S) the floored error is at most
+# (1 + 10^3) * 2^-24 = 6.0e-5.
+COLLAPSED_TOL = 1e-4
 
 
 def _check(got, expect, mag, tol, label):

@@ -72,6 +72,23 @@ MUTANTS = [
      "for (int i = 1; i < n - 1; ++i) {\n      for (int k = n - 1; k >= i; --k)", 0),
     ("table uses step not abscissa", "return oracle_weights_row(x, count, abscissa[s], w);",
      "return oracle_weights_row(x, count, abscissa[s] + 1.0, w);", 0),
+    # one planted mistake in each storage type's own sum (the occurrences of
+    # the sum line are the bf16, binary32 and binary16 versions, in that order)
+    ("bf16 sum pairs weight k-1 with entry k", "s += w[k] * f;", "s += w[k > 0 ? k - 1 : 0] * f;", 0),
+    ("f32 sum pairs weight k-1 with entry k", "s += w[k] * f;", "s += w[k > 0 ? k - 1 : 0] * f;", 1),
+    ("f16 sum pairs weight k-1 with entry k", "s += w[k] * f;", "s += w[k > 0 ? k - 1 : 0] * f;", 2),
+    ("f16 sum history reversed", "double f = oracle_f16_to_f64(F[k][i]);",
+     "double f = oracle_f16_to_f64(F[n - 1 - k][i]);", 0),
+    # the binary32 and binary16 residual checkers
+    ("residual f32 drops x_in", "x_out[j] = x_in ? x_in[j] : 0.0;", "x_out[j] = 0.0;", 1),
+    ("residual f32 reads the previous segment's slot", "double f = (double)F[k][slot_offset[s] + e];",
+     "double f = (double)F[k][slot_offset[s > 0 ? s - 1 : s] + e];", 0),
+    ("residual f16 decodes as bfloat16", "double f = oracle_f16_to_f64(F[k][slot_offset[s] + e]);",
+     "double f = oracle_bf16_to_f64(F[k][slot_offset[s] + e]);", 0),
+    ("residual f16 magnitude keeps the weight's sign", "mag += fabs(w[k]) * fabs(f);",
+     "mag += w[k] * fabs(f);", 2),
+    ("residual f16 skips the last covering segment", "for (int s = 0; s < n_segs; ++s) {\n    if (res_offset[s] < 0) continue;",
+     "for (int s = 0; s < n_segs - 1; ++s) {\n    if (res_offset[s] < 0) continue;", 2),
 ]
 
 
@@ -81,9 +98,11 @@ def _battery():
         if not name.startswith("test_"):
             continue
         fn = getattr(pins, name)
-        if name == "test_config_weights_equal_exact_lagrange":
-            for case in pins._all_config_cases():
-                tests.append((f"{name}[{case[0]}]", functools.partial(fn, case)))
+        marks = [m for m in getattr(fn, "pytestmark", []) if m.name == "parametrize"]
+        if marks:                       # one parameter: expand its values
+            argname, values = marks[0].args[0], marks[0].args[1]
+            for v in values:
+                tests.append((f"{name}[{v!r}]", functools.partial(fn, **{argname: v})))
         else:
             tests.append((name, fn))
     return tests

@@ -383,6 +383,91 @@ def test_round_f16_agrees_with_numpy():
     assert np.array_equal(oracle.round_f16(v), ref)
 
 
+# Storage encodings of small integers, made by torch and numpy (not by the
+# oracle), with the round trip checked: the polynomial pins below need the
+# stored values to be the integers themselves.
+_INT_LIMIT = {"bf16": 256, "f16": 2048, "f32": 1 << 24}
+
+
+def _encode_ints(vals, dtype):
+    v = np.asarray(vals, dtype=np.int64)
+    if dtype == "bf16":
+        t = torch.from_numpy(v.astype(np.float32)).to(torch.bfloat16)
+        assert torch.equal(t.double(), torch.from_numpy(v.astype(np.float64)))
+        return t.view(torch.int16).numpy().view(np.uint16)
+    if dtype == "f16":
+        h = v.astype(np.float16)
+        assert np.array_equal(h.astype(np.int64), v)
+        return h.view(np.uint16)
+    f = v.astype(np.float32)
+    assert np.array_equal(f.astype(np.int64), v)
+    return f
+
+
+def _extrapolate(dtype, entries, w):
+    fn = {"bf16": oracle.extrapolate_bf16, "f16": oracle.extrapolate_f16,
+          "f32": oracle.extrapolate_f32}[dtype]
+    return fn(entries, w)
+
+
+def _integer_polynomials(rng, nodes, deg, count, limit):
+    """Integer coefficient rows (count x (deg+1)) whose values at every node
+    are integers of magnitude <= limit (rejection sampling), and those values
+    (exact integer arithmetic)."""
+    X = np.array([[int(x) ** d for d in range(deg + 1)] for x in nodes], dtype=np.int64)
+    rows, vals = [], []
+    while sum(len(r) for r in rows) < count:
+        c = rng.integers(-4, 5, size=(4 * count, deg + 1))
+        v = c @ X.T
+        ok = np.all(np.abs(v) <= limit, axis=1)
+        rows.append(c[ok])
+        vals.append(v[ok])
+    return np.concatenate(rows)[:count], np.concatenate(vals)[:count]
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16", "f32"])
+def test_stored_polynomials_reproduced_by_each_storage_sum(dtype):
+    """Appendix A error term: a polynomial of degree <= K is its own
+    interpolant, so the prediction from K+1 stored node values is the
+    polynomial's value at the target.  Integer polynomials whose node values
+    are exact in the storage format; the expected value p(t) is Horner's rule
+    on the integer coefficients, in exact rationals.  Through each storage
+    type's own sum, equispaced and uneven integer nodes, degree up to K."""
+    from fractions import Fraction
+    rng = np.random.default_rng({"bf16": 101, "f16": 103, "f32": 107}[dtype])
+    node_sets = [[0, 1], [-1, 0, 1], [-1, 0, 1, 2], [-2, -1, 0, 1, 2], [-3, -1, 0, 2],
+                 [-2, -1, 0, 1, 2, 3], [-3, -2, 0, 1, 3]]
+    for nodes in node_sets:
+        K = len(nodes) - 1
+        for deg in sorted({0, K // 2, K}):
+            coef, vals = _integer_polynomials(rng, nodes, deg, 512, _INT_LIMIT[dtype])
+            entries = [_encode_ints(vals[:, k], dtype) for k in range(K + 1)]
+            for t in (max(nodes) + 1, max(nodes) + 2, max(nodes) + 0.5, min(nodes) - 1.5):
+                w = oracle.weights_row(nodes, t)
+                got, mag = _extrapolate(dtype, entries, w)
+                ft = Fraction(t)
+                want = np.array([float(sum(int(c) * ft ** d for d, c in enumerate(row)))
+                                 for row in coef])
+                tol = 64 * len(w) * 2.0 ** -53 * np.abs(w).sum() * (mag + np.abs(want)) + 1e-300
+                assert np.all(np.abs(got - want) <= tol), (dtype, nodes, deg, t)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16", "f32"])
+def test_newton_weights_on_stored_cubics_exact(dtype):
+    """Closed form with no weight computation: w = (-1, 4, -6, 4), the
+    fourth forward difference of a cubic being zero, predicts p(4) from
+    p(0..3) exactly for every integer cubic (all terms exact in fp64); the
+    magnitude is sum_k |w_k| |p(k)|."""
+    rng = np.random.default_rng(109)
+    coef, vals = _integer_polynomials(rng, [0, 1, 2, 3], 3, 400, _INT_LIMIT[dtype])
+    entries = [_encode_ints(vals[:, k], dtype) for k in range(4)]
+    w = np.array([-1.0, 4.0, -6.0, 4.0])
+    got, mag = _extrapolate(dtype, entries, w)
+    want = coef @ np.array([1, 4, 16, 64])
+    assert np.array_equal(got, want.astype(np.float64))
+    assert np.array_equal(mag, (np.abs(vals) @ np.abs(w)).astype(np.float64))
+
+
 def test_extrapolate_f16_decodes_exactly():
     rng = np.random.default_rng(43)
     vals = (rng.standard_normal((5, 2001)) * 3).astype(np.float16)
@@ -465,6 +550,61 @@ def test_residual_hand_worked():
                                x_in=[10.0, 20.0, 30.0, 40.0])
     assert out.tolist() == [11.0, 20.0, 28.0, 36.0]
     assert mag.tolist() == [13.0, 24.0, 44.0, 56.0]
+
+
+def test_residual_hand_worked_f32():
+    """binary32 entries (values that need all 24 significand bits),
+    w = [-1, 2], a 4-element residual: segment 0 (slot 0..3) adds at 0..3,
+    segment 1 (slot 4..5) at 1..2, overlapping it, segment 2 (slot 6..9) is
+    not added.  Per slot element p = -F0 + 2 F1:
+        p0..p5 = 0, 0.5 + 2^-19, 4, 2 - 2^-22, 2, -6
+    so x = [0, 2.5 + 2^-19, -2, 2 - 2^-22] without x_in; the magnitudes
+    |F0| + 2|F1| are 1, 3.5 + 2^-19, 4, 8 + 2^-22, 22, 34."""
+    u = 2.0 ** -22
+    F0 = np.array([0.5, 1.5, -2.0, 3.0 + u, 10.0, 20.0, 99.0, 99.0, 99.0, 99.0], np.float32)
+    F1 = np.array([0.25, 1.0 + 2.0 ** -20, 1.0, 2.5, 6.0, 7.0, 99.0, 99.0, 99.0, 99.0],
+                  np.float32)
+    assert float(F0[3]) == 3.0 + u and float(F1[1]) == 1.0 + 2.0 ** -20
+    kw = dict(slot_offset=[0, 4, 6], seg_numel=[4, 2, 4], res_offset=[0, 1, -1], res_numel=4,
+              dtype="f32")
+    out, mag = oracle.residual([F0, F1], [-1.0, 2.0], **kw)
+    assert out.tolist() == [0.0, 2.5 + 2.0 ** -19, -2.0, 2.0 - u]
+    assert mag.tolist() == [1.0, 25.5 + 2.0 ** -19, 38.0, 8.0 + u]
+    out, mag = oracle.residual([F0, F1], [-1.0, 2.0], x_in=[1.0, -1.0, 0.25, 100.0], **kw)
+    assert out.tolist() == [1.0, 1.5 + 2.0 ** -19, -1.75, 102.0 - u]
+    assert mag.tolist() == [2.0, 26.5 + 2.0 ** -19, 38.25, 108.0 + u]
+
+
+def test_residual_hand_worked_f16():
+    """binary16 entries with subnormals (2^-24, 3 * 2^-24), the smallest
+    normal 2^-14, an 11-bit significand (1 + 2^-10) and the largest finite
+    value 65504; three entries, w = [0.5, -1.5, 2]; segment 0 (slot 0..1)
+    adds at residual 2..3, segment 1 (slot 2..5) at 0..3, residual element
+    4 is covered by none.  Per slot element p = 0.5 F0 - 1.5 F1 + 2 F2:
+        p0 = 2^-13 - 2^-22, p1 = 3 + 2^-11, p2 = 1, p3 = 1, p4 = 1.875,
+        p5 = 31218,
+    so x = [1, 1, 1.875 + 2^-13 - 2^-22, 31221 + 2^-11, 0]; the magnitudes
+    0.5|F0| + 1.5|F1| + 2|F2| are 5 * 2^-24 + 2^-13, 6 + 2^-11, 7, 9, 2.625,
+    34290."""
+    bits = lambda v: np.array(v, dtype=np.uint16)
+    F0 = bits([0x0001, 0x3C01, 0x4400, 0xC800, 0x3800, 0x7BFF])   # 2^-24, 1+2^-10, 4, -8, .5, 65504
+    F1 = bits([0x0003, 0x3C00, 0x4000, 0xC000, 0x3400, 0x6400])   # 3*2^-24, 1, 2, -2, .25, 1024
+    F2 = bits([0x0400, 0x4000, 0x3C00, 0x3C00, 0x3C00, 0x3C00])   # 2^-14, 2, 1, 1, 1, 1
+    dec = [np.array(f).view(np.float16).astype(np.float64).tolist() for f in (F0, F1, F2)]
+    assert dec[0] == [2.0 ** -24, 1 + 2.0 ** -10, 4.0, -8.0, 0.5, 65504.0]
+    assert dec[1] == [3 * 2.0 ** -24, 1.0, 2.0, -2.0, 0.25, 1024.0]
+    assert dec[2] == [2.0 ** -14, 2.0, 1.0, 1.0, 1.0, 1.0]
+    kw = dict(slot_offset=[0, 2], seg_numel=[2, 4], res_offset=[2, 0], res_numel=5, dtype="f16")
+    w = [0.5, -1.5, 2.0]
+    out, mag = oracle.residual([F0, F1, F2], w, **kw)
+    assert out.tolist() == [1.0, 1.0, 1.875 + 2.0 ** -13 - 2.0 ** -22, 31221.0 + 2.0 ** -11, 0.0]
+    assert mag.tolist() == [7.0, 9.0, 2.625 + 5 * 2.0 ** -24 + 2.0 ** -13,
+                            34296.0 + 2.0 ** -11, 0.0]
+    x_in = [0.5, -0.5, 0.0, 2.0, 7.0]
+    out, mag = oracle.residual([F0, F1, F2], w, x_in=x_in, **kw)
+    assert out.tolist() == [1.5, 0.5, 1.875 + 2.0 ** -13 - 2.0 ** -22, 31223.0 + 2.0 ** -11, 7.0]
+    assert mag.tolist() == [7.5, 9.5, 2.625 + 5 * 2.0 ** -24 + 2.0 ** -13,
+                            34298.0 + 2.0 ** -11, 7.0]
 
 
 def test_residual_single_segment_is_the_prediction():
