@@ -20,7 +20,9 @@
  *   - Return value: CHEB_OK (0) or a negative cheb_status.  On failure,
  *     cheb_last_error() returns a message for the calling thread.  Every
  *     argument is checked on the host before anything is enqueued, so a
- *     failed call has enqueued no GPU work.
+ *     call refused for its arguments has enqueued no GPU work.  A call that
+ *     launches more than once can fail with CHEB_E_HIP after an earlier
+ *     launch went in; cheb_cache_push documents what it leaves behind.
  *   - Device memory (history arena, sources, outputs) belongs to the caller.
  *     The library never allocates or frees device memory.  It owns only the
  *     host-side handle returned by cheb_cache_create.
@@ -201,7 +203,24 @@ CHEB_API int cheb_combine_multi(const void *const *src, int32_t n_src, const dou
  * flat layout: segment s of the prediction is at out + seg_offset[s]. */
 typedef struct cheb_cache cheb_cache;
 
-/* Layout of a cache without creating it.
+/* Device bytes the history buffer H of n_slots entries needs (Section 3.3,
+ * forward application: a fixed-size buffer of the n most recent full
+ * steps; Algorithm 1: each full step stores (s, f_s) in H), so that the
+ * caller can allocate the arena before cheb_cache_create.
+ *   seg_numel         [n_segs] host, element counts of the cached tensors of
+ *                     one full step (each >= 0).
+ *   arena_bytes       out: bytes of the whole arena (n_slots slots).
+ *   slot_stride_bytes out: bytes from one slot to the next (a multiple of
+ *                     256); may be NULL.
+ * 1 <= n_slots <= CHEB_MAX_SLOTS, n_segs >= 1.  Errors: CHEB_E_INVAL,
+ * CHEB_E_DTYPE.  Nothing is written on error. */
+CHEB_API int cheb_cache_arena_bytes(int32_t n_slots, int32_t dtype, const int64_t *seg_numel,
+                                    int32_t n_segs, size_t *arena_bytes,
+                                    size_t *slot_stride_bytes);
+
+/* The whole layout of that buffer (Section 3.3; Algorithm 1, as
+ * cheb_cache_arena_bytes), also giving where each cached tensor lives in a
+ * slot and in an output.
  *   seg_numel  [n_segs] element counts (each >= 0).
  *   seg_offset [n_segs] out, may be NULL.
  *   slot_numel, slot_stride_bytes, arena_bytes: out, each may be NULL.
@@ -211,67 +230,93 @@ CHEB_API int cheb_cache_layout(int32_t n_slots, int32_t dtype, const int64_t *se
                       int32_t n_segs, int64_t *seg_offset, int64_t *slot_numel,
                       size_t *slot_stride_bytes, size_t *arena_bytes);
 
-/* Creates a handle over `arena` (device, 256-byte aligned, at least
- * arena_bytes of cheb_cache_layout).  The arena stays caller-owned and must
- * outlive the handle.  The history starts empty.  Errors: CHEB_E_INVAL,
- * CHEB_E_DTYPE, CHEB_E_ALIGN, CHEB_E_MISMATCH. */
+/* Creates the history buffer H of Section 3.3 (n = n_slots entries, empty
+ * at the start of sampling; Algorithm 1, online stage) over `arena`
+ * (device, 256-byte aligned, at least the bytes cheb_cache_arena_bytes
+ * gives).  The arena stays caller-owned and must outlive the handle.
+ * Errors: CHEB_E_INVAL, CHEB_E_DTYPE, CHEB_E_ALIGN, CHEB_E_MISMATCH. */
 CHEB_API int cheb_cache_create(cheb_cache **out, int32_t n_slots, int32_t dtype,
                       const int64_t *seg_numel, int32_t n_segs, void *arena,
                       size_t arena_bytes);
 
-/* Frees the handle (not the arena).  NULL is accepted. */
+/* Ends the history buffer H of Section 3.3 (Algorithm 1, end of the
+ * sampling loop): frees the handle, not the arena.  NULL is accepted. */
 CHEB_API int cheb_cache_destroy(cheb_cache *c);
 
-/* Empties the history (metadata only; arena contents are left as they are). */
+/* Empties H for a new sampling run (Algorithm 1 starts the online stage
+ * with an empty history): metadata only; arena contents are left as they
+ * are. */
 CHEB_API int cheb_cache_reset(cheb_cache *c);
 
 /* Stores the full step at abscissa t: copies segment s from seg_src[s]
  * (device, 16-byte aligned, seg_numel[s] elements) into the slot of the
  * oldest entry (or the next free one), zero-fills the padding after each
  * segment, records t and advances the ring (Algorithm 1, full computation:
- * store (s, f_s) in H).  One launch per 64 segments, asynchronous on
- * `stream`.  Errors: CHEB_E_INVAL, CHEB_E_NONFINITE, CHEB_E_DUPNODE (t already
- * held), CHEB_E_ALIGN, CHEB_E_NOTREADY (a fused push is open), CHEB_E_HIP. */
+ * store (s, f_s) in H; Section 3.3, the oldest entry is evicted).  One
+ * launch per 64 segments, asynchronous on `stream`.
+ * A launch failure (CHEB_E_HIP) after the arguments were accepted leaves
+ * the history without the entry whose slot the copy was writing: a full
+ * ring has dropped its oldest entry (the launches before the failing one
+ * may have overwritten part of its slot), a ring with a free slot is as
+ * before, and t is not recorded.  Every other held entry is untouched, so
+ * a later prediction never reads a half-written slot.
+ * Errors: CHEB_E_INVAL, CHEB_E_NONFINITE, CHEB_E_DUPNODE (t already held),
+ * CHEB_E_ALIGN, CHEB_E_NOTREADY (a fused push is open), CHEB_E_HIP. */
 CHEB_API int cheb_cache_push(cheb_cache *c, double t, const void *const *seg_src,
                     void *stream);
 
-/* Fused push, part 1: returns in *slot_base the device address of the slot
- * the next entry will occupy, so the full step can write its outputs there
- * directly (segment s at slot_base + seg_offset[s] elements).  The entry that
- * slot held is dropped from the history at once.  Until cheb_cache_commit,
- * pushes and extrapolations fail with CHEB_E_NOTREADY.  Errors: CHEB_E_INVAL,
+/* Fused push, part 1 (Algorithm 1, full computation: store (s, f_s) in H;
+ * Section 3.3, the oldest entry is evicted): returns in *slot_base the
+ * device address of the slot the next entry will occupy, so the full step
+ * can write its outputs there directly (segment s at slot_base +
+ * seg_offset[s] elements).  The entry that slot held is dropped from the
+ * history at once.  The library writes nothing into the slot: the padding
+ * after each segment keeps whatever the slot held, so the padding elements
+ * of later predictions are unspecified (they may be NaN); every segment's
+ * own elements are exact.  Until cheb_cache_commit, pushes and
+ * extrapolations fail with CHEB_E_NOTREADY.  Errors: CHEB_E_INVAL,
  * CHEB_E_NOTREADY (already open). */
 CHEB_API int cheb_cache_begin_push(cheb_cache *c, void **slot_base);
 
-/* Fused push, part 2: records abscissa t for the open slot (metadata only;
- * no GPU work).  The caller orders the writes into the slot before any later
+/* Fused push, part 2 (Algorithm 1, full computation: store (s, f_s) in H):
+ * records abscissa t for the open slot (metadata only; no GPU work).  The caller orders the writes into the slot before any later
  * use of the cache on its streams.  Errors: CHEB_E_INVAL, CHEB_E_NONFINITE,
  * CHEB_E_DUPNODE, CHEB_E_NOTREADY (no push open). */
 CHEB_API int cheb_cache_commit(cheb_cache *c, double t);
 
-/* Fused push, abandoned: closes the open push without recording an entry
+/* Fused push, abandoned (Algorithm 1 stores only completed full steps in
+ * H): closes the open push without recording an entry
  * (for a full step that failed before its outputs were complete).  The
  * entry that slot held stays dropped, so a full ring holds one entry fewer
  * afterwards; the others are untouched.  Errors: CHEB_E_INVAL,
  * CHEB_E_NOTREADY (no push open). */
 CHEB_API int cheb_cache_abort_push(cheb_cache *c);
 
-/* Abscissae held, oldest to newest: t_out[0 .. *count-1] (t_out has room for
- * n_slots values; it may be NULL).  Errors: CHEB_E_INVAL. */
+/* The abscissae s_j held in H (Section 3.3; Algorithm 1), oldest to newest,
+ * the order the weight rows of cheb_precompute_weights and
+ * cheb_extrapolate use: t_out[0 .. *count-1] (t_out has room for n_slots
+ * values; it may be NULL).  Errors: CHEB_E_INVAL. */
 CHEB_API int cheb_cache_history(const cheb_cache *c, double *t_out, int32_t *count);
 
-/* Device address of the entry of age index `idx` (0 = oldest held).
- * Errors: CHEB_E_INVAL (idx outside 0 .. count-1). */
+/* Device address of the features f_{s_j} of held entry j (Section 3.3;
+ * Algorithm 1), j = `idx` counted from the oldest (0).  Errors:
+ * CHEB_E_INVAL (idx outside 0 .. count-1). */
 CHEB_API int cheb_cache_entry(const cheb_cache *c, int32_t idx, void **slot_base);
 
-/* Element offset of segment `seg` in a slot and in an output buffer. */
+/* Element offset of cached tensor `seg` (one module output of the block
+ * equation of Section 3.1) in a slot of H and in a prediction output
+ * (Section 3.3, forward application: the prediction has the layout of the
+ * features it combines).  Errors: CHEB_E_INVAL. */
 CHEB_API int cheb_cache_segment_offset(const cheb_cache *c, int32_t seg,
                               int64_t *elem_offset);
 
-/* Storage type (cheb_dtype) of the cache. */
+/* Storage type (cheb_dtype) of the entries of H and of its predictions
+ * (Section 3.3).  Errors: CHEB_E_INVAL. */
 CHEB_API int cheb_cache_dtype(const cheb_cache *c, int32_t *dtype);
 
-/* Elements of one slot (= elements an output buffer must hold). */
+/* Elements of one entry of H, which is also the element count of one
+ * prediction output (Section 3.3, forward application).  Errors:
+ * CHEB_E_INVAL. */
 CHEB_API int cheb_cache_slot_numel(const cheb_cache *c, int64_t *numel);
 
 /* The skipped-step prediction (Section 3.3, forward application equation;

@@ -16,7 +16,7 @@ from ._binding import (  # noqa: F401  (re-exported C entry points)
     CHEB_BF16, CHEB_F16, CHEB_F32, CHEB_MAX_NODES, CHEB_MAX_OUTPUTS, CHEB_MAX_SLOTS, CHEB_RHO_ALTERNATING,
     CHEB_RHO_GENERAL, CHEB_SHORT_FULL, CHEB_TAYLOR, CHEB_SHORT_LOWER, ChebError, cheb_chebyshev_nodes,
     cheb_precompute_weights_variant,
-    cheb_cache_abort_push, cheb_cache_begin_push, cheb_cache_commit, cheb_cache_create,
+    cheb_cache_abort_push, cheb_cache_arena_bytes, cheb_cache_begin_push, cheb_cache_commit, cheb_cache_create,
     cheb_cache_destroy,
     cheb_cache_dtype, cheb_cache_entry, cheb_cache_history, cheb_cache_layout, cheb_cache_push,
     cheb_cache_reset, cheb_cache_segment_offset, cheb_cache_slot_numel, cheb_combine,

@@ -77,6 +77,7 @@ SIGNATURES = {
     "cheb_combine": [_vpp, ctypes.c_int32, _dp, _vp, ctypes.c_int64, ctypes.c_int32, _vp],
     "cheb_combine_multi": [_vpp, ctypes.c_int32, _dp, ctypes.c_int32, _vpp, ctypes.c_int64,
                            ctypes.c_int32, _vp],
+    "cheb_cache_arena_bytes": [ctypes.c_int32, ctypes.c_int32, _i64p, ctypes.c_int32, _szp, _szp],
     "cheb_cache_layout": [ctypes.c_int32, ctypes.c_int32, _i64p, ctypes.c_int32, _i64p,
                           _i64p, _szp, _szp],
     "cheb_cache_create": [ctypes.POINTER(_vp), ctypes.c_int32, ctypes.c_int32, _i64p,
@@ -195,6 +196,16 @@ def cheb_combine_multi(src_ptrs, w, out_ptrs, numel, dtype, stream=0):
     _check(LIB.cheb_combine_multi(_voidp_array(src_ptrs), len(src_ptrs), _dptr(w), n_out,
                                   _voidp_array(out_ptrs), int(numel), int(dtype),
                                   ctypes.c_void_p(int(stream))))
+
+
+def cheb_cache_arena_bytes(n_slots, dtype, seg_numel):
+    """(arena_bytes, slot_stride_bytes) of a history of n_slots entries."""
+    seg = np.ascontiguousarray(seg_numel, dtype=np.int64).reshape(-1)
+    arena = ctypes.c_size_t()
+    stride = ctypes.c_size_t()
+    _check(LIB.cheb_cache_arena_bytes(int(n_slots), int(dtype), seg.ctypes.data_as(_i64p),
+                                      seg.size, ctypes.byref(arena), ctypes.byref(stride)))
+    return arena.value, stride.value
 
 
 def cheb_cache_layout(n_slots, dtype, seg_numel):

@@ -134,6 +134,19 @@ int cache_view(const cheb_cache *c, CacheView *v) {
 
 extern "C" {
 
+int cheb_cache_arena_bytes(int32_t n_slots, int32_t dtype, const int64_t *seg_numel,
+                           int32_t n_segs, size_t *arena_bytes, size_t *slot_stride_bytes) {
+  if (!arena_bytes) return fail(CHEB_E_INVAL, "arena_bytes is NULL");
+  std::vector<int64_t> off;
+  int64_t sn = 0;
+  size_t st = 0, ab = 0;
+  int rc = layout(n_slots, dtype, seg_numel, n_segs, &off, &sn, &st, &ab);
+  if (rc != CHEB_OK) return rc;
+  *arena_bytes = ab;
+  if (slot_stride_bytes) *slot_stride_bytes = st;
+  return ok();
+}
+
 int cheb_cache_layout(int32_t n_slots, int32_t dtype, const int64_t *seg_numel, int32_t n_segs,
                       int64_t *seg_offset, int64_t *slot_numel, size_t *slot_stride_bytes,
                       size_t *arena_bytes) {
@@ -206,12 +219,13 @@ int cheb_cache_push(cheb_cache *c, double t, const void *const *seg_src, void *s
     segs[s] = GatherSeg{seg_src[s], c->seg_offset[s], c->seg_numel[s]};
   }
   // The entry goes to slot `head`: the next free slot, or the oldest entry's
-  // slot when the ring is full.
-  const int32_t slot = c->head;
+  // slot when the ring is full.  That entry leaves the history before the
+  // first launch, so a launch that fails after an earlier one has written
+  // part of the slot cannot leave a half-overwritten entry in the history.
+  const int32_t slot = claim_slot(c);
   rc = launch_gather(c->dtype, c->slot_ptr(slot), segs.data(), int(n_segs),
                      static_cast<hipStream_t>(stream));
   if (rc != CHEB_OK) return rc;
-  claim_slot(c);
   record(c, t);
   return ok();
 }

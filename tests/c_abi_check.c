@@ -37,6 +37,13 @@ int main(int argc, char **argv) {
   CHECK(cheb_cache_layout(4, CHEB_BF16, seg, 3, off, &slot_numel, &stride, &arena) == CHEB_OK);
   CHECK(off[0] == 0 && off[1] == 16 && off[2] == 24 && slot_numel == 24 + 4096);
   CHECK(stride % 256 == 0 && arena == 4 * stride);
+  size_t arena2 = 0, stride2 = 0;
+  CHECK(cheb_cache_arena_bytes(4, CHEB_BF16, seg, 3, &arena2, &stride2) == CHEB_OK);
+  CHECK(arena2 == arena && stride2 == stride);
+  CHECK(cheb_cache_arena_bytes(4, CHEB_BF16, seg, 3, &arena2, NULL) == CHEB_OK && arena2 == arena);
+  CHECK(cheb_cache_arena_bytes(0, CHEB_BF16, seg, 3, &arena2, &stride2) == CHEB_E_INVAL);
+  CHECK(cheb_cache_arena_bytes(4, 7, seg, 3, &arena2, &stride2) == CHEB_E_DTYPE);
+  CHECK(cheb_cache_arena_bytes(4, CHEB_BF16, seg, 3, NULL, &stride2) == CHEB_E_INVAL);
 
   /* A handle over an address that is never dereferenced: metadata only. */
   void *fake = (void *)(uintptr_t)((uint64_t)1 << 40);

@@ -80,6 +80,12 @@ int main(void) {
   size_t stride = 0, arena_bytes = 0;
   CHECK_CHEB(cheb_cache_layout(N_SLOTS, CHEB_BF16, seg_numel, N_SEGS, seg_offset, &slot_numel,
                                &stride, &arena_bytes));
+  size_t arena_bytes2 = 0;
+  CHECK_CHEB(cheb_cache_arena_bytes(N_SLOTS, CHEB_BF16, seg_numel, N_SEGS, &arena_bytes2, NULL));
+  if (arena_bytes2 != arena_bytes) {
+    fprintf(stderr, "arena bytes disagree: %zu vs %zu\n", arena_bytes2, arena_bytes);
+    return 1;
+  }
   void *arena = NULL;
   CHECK_HIP(hipMalloc(&arena, arena_bytes));
   cheb_cache *cache = NULL;

@@ -30,8 +30,10 @@ def _declared():
 
 def test_header_declares_expected_entry_points():
     names = _declared()
-    for must in ("cheb_precompute_weights", "cheb_cache_push", "cheb_extrapolate",
-                 "cheb_cache_create", "cheb_last_error"):
+    for must in ("cheb_precompute_weights", "cheb_cache_arena_bytes", "cheb_cache_create",
+                 "cheb_cache_push", "cheb_cache_begin_push", "cheb_cache_commit",
+                 "cheb_cache_history", "cheb_cache_segment_offset", "cheb_extrapolate",
+                 "cheb_cache_destroy", "cheb_last_error"):
         assert must in names
     assert len(names) == len(B.SIGNATURES)
 
@@ -188,6 +190,7 @@ def test_layout_rounding(dtype, esize):
     assert lay["slot_numel"] == pos
     assert lay["slot_stride_bytes"] == stride and stride % 256 == 0
     assert lay["arena_bytes"] == arena
+    assert cheb.cheb_cache_arena_bytes(5, dtype, seg) == (arena, stride)
 
 
 def test_layout_of_workloads_has_no_padding():
@@ -204,6 +207,9 @@ def test_layout_errors():
                        ((2, 0, [1 << 40]), B.CHEB_E_INVAL)]:
         with pytest.raises(cheb.ChebError) as e:
             cheb.cheb_cache_layout(*args)
+        assert e.value.code == code
+        with pytest.raises(cheb.ChebError) as e:
+            cheb.cheb_cache_arena_bytes(*args)
         assert e.value.code == code
 
 

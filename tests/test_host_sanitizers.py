@@ -65,3 +65,33 @@ def test_host_code_under_tsan(tmp_path):
     assert r.returncode == 0, r.stdout + r.stderr
     assert "threads ok" in r.stdout
     assert "WARNING: ThreadSanitizer" not in r.stderr, r.stderr
+
+
+@pytest.mark.skipif(shutil.which("g++") is None, reason="needs g++")
+def test_failed_push_leaves_no_half_written_entry(tmp_path):
+    """A copy push into a full ring whose second segment-copy launch fails
+    (host stubs that let a set number of launches succeed): the history no
+    longer lists the entry being overwritten, predictions report NOTREADY,
+    and the next push reuses the slot.  Under ASan and UBSan, CPU only."""
+    san = ["-fsanitize=address,undefined", "-fno-sanitize-recover=undefined",
+           "-fno-omit-frame-pointer", "-g", "-O1"]
+    inc = ["-I", os.path.join(ROOT, "include"), "-I", CSRC, "-I", os.path.join(ROCM, "include")]
+    objs = []
+    for src in HOST_SOURCES + ["host_stubs.cpp"]:
+        path = os.path.join(HERE if src == "host_stubs.cpp" else CSRC, src)
+        obj = os.path.join(tmp_path, src + ".o")
+        subprocess.run(["g++", "-std=c++17", "-D__HIP_PLATFORM_AMD__", *san, *inc, "-c", path,
+                        "-o", obj], check=True)
+        objs.append(obj)
+    cobj = os.path.join(tmp_path, "push_failure_check.o")
+    subprocess.run(["gcc", "-std=c99", *san, "-I", os.path.join(ROOT, "include"), "-c",
+                    os.path.join(HERE, "push_failure_check.c"), "-o", cobj], check=True)
+    exe = os.path.join(tmp_path, "push_failure_check")
+    libdir = os.path.join(ROCM, "lib")
+    subprocess.run(["g++", *san, cobj, *objs, "-o", exe, "-L", libdir, "-lamdhip64",
+                    f"-Wl,-rpath,{libdir}", "-lm"], check=True)
+    env = dict(os.environ, ASAN_OPTIONS="detect_leaks=1:abort_on_error=1",
+               UBSAN_OPTIONS="print_stacktrace=1:halt_on_error=1")
+    r = subprocess.run([exe], capture_output=True, text=True, env=env, timeout=120)
+    assert r.returncode == 0, r.stdout + r.stderr
+    assert "push failure ok" in r.stdout
