@@ -5,9 +5,12 @@ A step is one skipped diffusion step: readiness check and weight row for the
 target (host, fp64) plus the prediction of every cached module output (one
 launch of the streaming kernel) over the FLUX.1-dev 1024x1024 feature cache
 (19 x [1,4096,3072] + 19 x [1,512,3072] + 38 x [1,4608,3072] bf16, six
-history entries).  Inputs are seeded synthetic features already resident in
-HBM.  The history is filled once before timing through the full-step push,
-which is timed on its own and reported beside the step.
+history entries) held in the interleaved layout (32 KiB chunks of the six
+entries taken in turn).  Inputs are seeded synthetic features already
+resident in HBM.  The history is filled once before timing through the
+full-step push, which is timed on its own and reported beside the step.
+The same step over the slot layout, and trivial-body streams with the same
+access patterns (the ceilings), are timed in the same run.
 
 Prints one JSON line.  Throughput counts algorithmic bytes: (K+1) entries read
 plus one output written, per step.
@@ -28,6 +31,8 @@ METRIC = "achieved HBM GB/s and µs per skipped step, FLUX-1024 cache shape, 1 M
 PEAK_HBM_GBPS = 8000.0
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2608_23429_amd", "csrc", "kernels.hip")
 PROFILES = os.path.join(ROOT, "profiles")
+CEILING_LIB = os.path.join(ROOT, "bench_ceiling.so")
+LAYOUT = "interleaved"
 
 
 def log(msg):
@@ -42,7 +47,7 @@ def kernel_sha256():
 def measured_traffic(workload):
     """HBM bytes per launch from committed rocprofv3 counter runs, if they
     were taken on the current kernel source; else None."""
-    path = os.path.join(PROFILES, f"traffic_extrapolate_{workload}.md")
+    path = os.path.join(PROFILES, f"traffic_extrapolate_{workload}_{LAYOUT}.md")
     if not os.path.exists(path):
         return None
     text = open(path).read()
@@ -68,6 +73,9 @@ def parse_args(argv=None):
                     help="approximate CPU time budget of the oracle baseline")
     ap.add_argument("--no-other-configs", dest="other_configs", action="store_false",
                     help="skip timing the other four workloads (per_config)")
+    ap.add_argument("--no-slots", dest="slots", action="store_false",
+                    help="time only the interleaved layout (no slot-layout comparison, no "
+                         "ceilings): for profiler runs that attribute dispatches by kernel")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain device copy of known size (counter calibration)")
     return ap.parse_args(argv)
@@ -91,16 +99,18 @@ def copy_probe(torch):
                       "ms": ms, "gbps": 2 * nbytes / ms / 1e6}), flush=True)
 
 
-def setup_workload(torch, cheb, cfg):
-    """Seeded history on the device, pushed through the ring."""
+def setup_workload(torch, cheb, cfg, layout, entries=None):
+    """Seeded history on the device (generated unless given), pushed through
+    the ring of a cache in `layout`."""
     from synth import make_history, split_segments
     dt = {"bf16": torch.bfloat16, "f16": torch.float16, "f32": torch.float32}[cfg.dtype]
-    t0 = time.time()
-    entries = make_history(cfg, "cuda")
-    torch.cuda.synchronize()
-    log(f"[bench] {cfg.name}: generated {cfg.n_hist} x {cfg.numel} elements "
-        f"in {time.time() - t0:.1f} s")
-    cache = cheb.ChebCache(cfg.n_hist, dt, cfg.seg_numel)
+    if entries is None:
+        t0 = time.time()
+        entries = make_history(cfg, "cuda")
+        torch.cuda.synchronize()
+        log(f"[bench] {cfg.name}: generated {cfg.n_hist} x {cfg.numel} elements "
+            f"in {time.time() - t0:.1f} s")
+    cache = cheb.ChebCache(cfg.n_hist, dt, cfg.seg_numel, layout=layout)
     stream = torch.cuda.current_stream()
     handle = int(stream.cuda_stream)
     # Segment addresses are gathered before the timed region, so the events
@@ -259,7 +269,7 @@ def time_online_run(torch, cheb, cfg, entries, reps=3):
     predicted = [table.step(s)[0] for s in range(T)]
     runs = dict(table.runs())
     dt = {"bf16": torch.bfloat16, "f16": torch.float16, "f32": torch.float32}[cfg.dtype]
-    cache = cheb.ChebCache(n, dt, cfg.seg_numel)
+    cache = cheb.ChebCache(n, dt, cfg.seg_numel, layout=LAYOUT)
     outs = [cache.new_output() for _ in range(max(runs.values()))]
     segs = [split_segments(e, cfg) for e in entries]
     res_off, res_n = cfg.residual_map()
@@ -438,7 +448,7 @@ def time_rotated(torch, cheb, cfg, entries, sets=32, steps=64):
     dt = {"bf16": torch.bfloat16, "f16": torch.float16, "f32": torch.float32}[cfg.dtype]
     pairs = []
     for _ in range(sets):
-        c = cheb.ChebCache(cfg.n_hist, dt, cfg.seg_numel)
+        c = cheb.ChebCache(cfg.n_hist, dt, cfg.seg_numel, layout=LAYOUT)
         for x, e in zip(cfg.nodes, entries):
             c.push(x, split_segments(e, cfg))
         pairs.append((c, c.new_output()))
@@ -450,14 +460,20 @@ def time_rotated(torch, cheb, cfg, entries, sets=32, steps=64):
     return us, sets * (cfg.n_hist + 1) * cfg.numel * cfg.elem_size
 
 
-def measure_config(torch, cheb, cfg, steps, warmup):
-    entries, cache, push_ms = setup_workload(torch, cheb, cfg)
+def measure_config(torch, cheb, cfg, steps, warmup, layout=LAYOUT, entries=None):
+    entries, cache, push_ms = setup_workload(torch, cheb, cfg, layout, entries)
     out = cache.new_output()
+    res = measure_cache(torch, cheb, cfg, cache, out, push_ms, entries, steps, warmup, layout)
+    return res, entries, cache, out
+
+
+def measure_cache(torch, cheb, cfg, cache, out, push_ms, entries, steps, warmup, layout):
     region_ms, per = time_steps(torch, cache, cfg.targets, out, steps, warmup)
     avg_launch_ms = sum(per) / len(per)
     B = cfg.bytes_per_step
     res = {
-        "workload": cfg.name, "elements": cfg.numel, "history": cfg.n_hist, "dtype": cfg.dtype,
+        "workload": cfg.name, "layout": layout, "elements": cfg.numel, "history": cfg.n_hist,
+        "dtype": cfg.dtype,
         "bytes_per_step": B, "us_per_step": region_ms * 1e3,
         "gbps": B / (region_ms * 1e6), "frac_of_8tbps": B / (region_ms * 1e6) / PEAK_HBM_GBPS,
         "launch_us_median": per[len(per) // 2] * 1e3, "launch_us_p10": per[len(per) // 10] * 1e3,
@@ -465,7 +481,7 @@ def measure_config(torch, cheb, cfg, steps, warmup):
         "push_us_median": sorted(push_ms)[len(push_ms) // 2] * 1e3,
         "push_gbps": 2 * cfg.numel * cfg.elem_size / (sorted(push_ms)[len(push_ms) // 2] * 1e6),
     }
-    if region_ms < 0.05:      # launch-bound: also time the steps replayed from a HIP graph
+    if region_ms < 0.05 and layout == LAYOUT:   # launch-bound: also replay from a HIP graph
         g_us = time_graph(torch, [(cache, out)], cfg.targets, 64)
         res["graph_us_per_step"] = g_us
         res["graph_gbps"] = B / (g_us * 1e3)
@@ -474,7 +490,60 @@ def measure_config(torch, cheb, cfg, steps, warmup):
                               "working_set_bytes": r_bytes,
                               "note": "graph-replayed steps cycling over 32 history copies "
                                       "(working set above the 256 MB last-level cache)"}
-    return res, entries, cache, out
+    return res
+
+
+def stream_ceilings(torch, slots_cache, il_cache, out, reps=10, warmup=2):
+    """Trivial-body streams (bench_ceiling.hip) over the benchmark's own
+    buffers, one entry-sized stream each, timed per launch with HIP events on
+    the current stream: six entries read, a copy, a write, and six entries
+    read with one stream written from the slot layout and from the
+    interleaved layout.  GB/s counts the bytes each kernel moves."""
+    import ctypes
+    lib = ctypes.CDLL(CEILING_LIB)
+    lib.ceiling_stream.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_void_p), ctypes.c_int,
+                                   ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
+    lib.ceiling_stream.restype = ctypes.c_int
+    import paper_2608_23429_amd as cheb
+    stream = torch.cuda.current_stream()
+    handle = int(stream.cuda_stream)
+    n = slots_cache.n_slots
+    S = slots_cache.slot_numel * torch.empty((), dtype=slots_cache.dtype).element_size()
+    n_vec = S // 16
+    slots = [slots_cache.arena.data_ptr() + k * slots_cache.slot_stride_bytes for k in range(n)]
+    # the interleaved region starts at its lowest lane
+    region = min(cheb.cheb_cache_entry(il_cache.handle, a) for a in range(n))
+    cases = [
+        ("read_only_6", 0, slots, n * S),
+        ("copy", 1, slots[:1], 2 * S),
+        ("write_only", 3, [], S),
+        ("mix_6_1_slots", 1, slots, (n + 1) * S),
+        ("mix_6_1_interleaved", 2, [region], (n + 1) * S),
+    ]
+    res = {}
+    for name, kind, src, nbytes in cases:
+        arr = (ctypes.c_void_p * max(1, len(src)))(*src) if src else None
+        n_src = n if kind == 2 else max(1, len(src))
+        def launch():
+            rc = lib.ceiling_stream(kind, arr, n_src, out.data_ptr(), n_vec, handle)
+            if rc != 0:
+                raise RuntimeError(f"ceiling_stream({name}) returned {rc}")
+        for _ in range(warmup):
+            launch()
+        torch.cuda.synchronize()
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(reps)]
+        for a, b in evs:
+            a.record(stream)
+            launch()
+            b.record(stream)
+        torch.cuda.synchronize()
+        ms = sorted(a.elapsed_time(b) for a, b in evs)
+        res[name] = {"bytes": nbytes, "us_median": ms[len(ms) // 2] * 1e3, "us_best": ms[0] * 1e3,
+                     "gbps_median": nbytes / (ms[len(ms) // 2] * 1e6),
+                     "gbps_best": nbytes / (ms[0] * 1e6)}
+        log(f"[bench] ceiling {name}: {res[name]['gbps_median']:.0f} GB/s median")
+    return res
 
 
 def main(argv=None):
@@ -507,8 +576,33 @@ def main(argv=None):
     cfg = by_name(args.config)
     log(f"[bench] workload {cfg.name}, launch shape {shape}, "
         f"{args.warmup} warmup + {args.steps} timed steps")
-    res, entries, cache, out = measure_config(torch, cheb, cfg, args.steps, args.warmup)
-    log(f"[bench] {cfg.name}: {res['us_per_step']:.1f} us/step, {res['gbps']:.0f} GB/s")
+    # Both layouts' caches are filled first; an untimed settle phase then runs
+    # the step on both for about a tenth of a second so that the first timed
+    # layout does not pay for the GPU's ramp from idle.  Then each layout:
+    # W warmup steps and K timed steps.
+    entries, cache, push_ms = setup_workload(torch, cheb, cfg, LAYOUT)
+    out = cache.new_output()
+    if args.slots:
+        _, cache_sl, push_sl = setup_workload(torch, cheb, cfg, "slots", entries)
+        out_sl = cache_sl.new_output()
+    for _ in range(25):
+        cache.extrapolate_at(cfg.targets[0], out)
+        if args.slots:
+            cache_sl.extrapolate_at(cfg.targets[0], out_sl)
+    torch.cuda.synchronize()
+    res = measure_cache(torch, cheb, cfg, cache, out, push_ms, entries, args.steps, args.warmup,
+                        LAYOUT)
+    log(f"[bench] {cfg.name} ({LAYOUT}): {res['us_per_step']:.1f} us/step, {res['gbps']:.0f} GB/s")
+    res_sl, ceilings = None, None
+    if args.slots:
+        res_sl = measure_cache(torch, cheb, cfg, cache_sl, out_sl, push_sl, entries, args.steps,
+                               args.warmup, "slots")
+        log(f"[bench] {cfg.name} (slots): {res_sl['us_per_step']:.1f} us/step, "
+            f"{res_sl['gbps']:.0f} GB/s")
+        ceilings = stream_ceilings(torch, cache_sl, cache, out_sl)
+        cache_sl.close()
+        del cache_sl, out_sl
+        torch.cuda.empty_cache()
     multi = time_multi(torch, cfg, cache, max(10, args.steps // 2), args.warmup)
     log(f"[bench] {cfg.name} multi-target: {multi['us_per_skipped_step']:.1f} us per skipped "
         f"step ({multi['gbps']:.0f} GB/s over {multi['targets_per_pass']} targets)")
@@ -524,6 +618,7 @@ def main(argv=None):
         f"{resid['collapsed_push_difference']['us']:.1f} us) per full step")
     achieved = res["bytes_per_step"] / (res["launch_us_avg"] * 1e3)
     traffic = measured_traffic(cfg.name)
+    own = ceilings["mix_6_1_interleaved"]["gbps_median"] if ceilings else None
     line = {
         "metric": METRIC,
         "value": res["gbps"],
@@ -542,9 +637,23 @@ def main(argv=None):
         "config": {"workload": cfg.name, "elements_per_entry": cfg.numel,
                    "history_entries": cfg.n_hist, "segments": len(cfg.segments),
                    "bytes_per_step": res["bytes_per_step"], "launch": shape,
-                   "parallelism": "single GPU"},
+                   "layout": LAYOUT, "parallelism": "single GPU"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBPS,
-                     "unit": "GB/s", "frac": achieved / PEAK_HBM_GBPS, "traffic": traffic},
+                     "unit": "GB/s", "frac": achieved / PEAK_HBM_GBPS, "traffic": traffic,
+                     "layout": LAYOUT,
+                     "ceiling": ceilings,
+                     "frac_of_ceiling": achieved / own if own else None,
+                     "ceiling_note": "trivial-body streams (XOR, same launch shape and access "
+                                     "pattern) over entry-sized streams of this workload, timed "
+                                     "in this run; frac_of_ceiling is against the 6-read:1-write "
+                                     "stream over the same interleaved layout"},
+        "layouts": {
+            LAYOUT: {"us_per_step": res["us_per_step"], "gbps": res["gbps"],
+                     "launch_us_avg": res["launch_us_avg"], "push_us_median": res["push_us_median"]},
+            "slots": None if res_sl is None else {
+                "us_per_step": res_sl["us_per_step"], "gbps": res_sl["gbps"],
+                "launch_us_avg": res_sl["launch_us_avg"], "push_us_median": res_sl["push_us_median"],
+                "note": "contiguous entries (the layout a fused push writes into)"}},
         "launch_us": {"median": res["launch_us_median"], "p10": res["launch_us_p10"],
                       "p90": res["launch_us_p90"], "avg": res["launch_us_avg"]},
         "push": {"us_median": res["push_us_median"], "gbps": res["push_gbps"],
@@ -574,9 +683,19 @@ def main(argv=None):
                 continue
             r, e, ch, o = measure_config(torch, cheb, c, max(10, args.steps // 2), args.warmup)
             log(f"[bench] {c.name}: {r['us_per_step']:.1f} us/step, {r['gbps']:.0f} GB/s")
-            per.append(r)
             ch.close()
-            del e, ch, o
+            del ch, o
+            if args.slots:
+                rs, _, ch, o = measure_config(torch, cheb, c, max(10, args.steps // 2),
+                                              args.warmup, layout="slots", entries=e)
+                log(f"[bench] {c.name} (slots): {rs['us_per_step']:.1f} us/step, "
+                    f"{rs['gbps']:.0f} GB/s")
+                r["slots"] = {"us_per_step": rs["us_per_step"], "gbps": rs["gbps"],
+                              "launch_us_avg": rs["launch_us_avg"]}
+                ch.close()
+                del ch, o
+            per.append(r)
+            del e
             torch.cuda.empty_cache()
         line["per_config"] = per
         shares = []

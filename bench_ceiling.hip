@@ -1,0 +1,114 @@
+// Stream ceilings of the benchmark (gfx950): trivial-body kernels with the
+// access pattern of the skipped-step prediction, timed in the same run as
+// the prediction so that its bandwidth can be read against what the chip
+// sustains for the same mix of reads and writes.
+//
+// Every kernel moves 16-byte vectors with non-temporal loads and stores, one
+// vector per lane, 1024-lane blocks, one block per 1024 vectors: the launch
+// shape the prediction uses.  The body is an XOR of the loaded vectors, so
+// arithmetic costs nothing.
+//   kind 0  read n_src contiguous streams, no store (a store that the data
+//           never triggers keeps the loads alive)
+//   kind 1  read n_src contiguous streams, write one stream
+//   kind 2  read n_src chunk-interleaved lanes of one region (32 KiB chunks,
+//           lane k of chunk c at (c * n_src + k) chunks from src[0]), write
+//           one contiguous stream
+//   kind 3  write one stream
+// Built by __graft_entry__.build() into bench_ceiling.so beside this file;
+// only bench.py loads it.
+#include <hip/hip_runtime.h>
+
+#include <stdint.h>
+
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kBlock = 1024;
+constexpr int kChunkShift = 11;  // 2048 vectors = 32 KiB
+constexpr uint32_t kChunkVecs = 1u << kChunkShift;
+
+struct Srcs {
+  const u32x4 *p[8];
+};
+
+template <int NS, int KIND>
+__global__ __launch_bounds__(kBlock) void stream_kernel(Srcs s, u32x4 *__restrict__ dst,
+                                                        uint32_t n_vec) {
+  const uint32_t i = blockIdx.x * uint32_t(kBlock) + threadIdx.x;
+  if (i >= n_vec) return;
+  u32x4 x = {i, 0u, 0u, 0u};
+  if constexpr (KIND != 3) {
+    u32x4 v[NS];
+    if constexpr (KIND == 2) {
+      const uint64_t base = uint64_t(i >> kChunkShift) * uint64_t(NS) * kChunkVecs +
+                            (i & (kChunkVecs - 1));
+#pragma unroll
+      for (int k = 0; k < NS; ++k)
+        v[k] = __builtin_nontemporal_load(s.p[0] + base + uint64_t(k) * kChunkVecs);
+    } else {
+#pragma unroll
+      for (int k = 0; k < NS; ++k) v[k] = __builtin_nontemporal_load(s.p[k] + i);
+    }
+    x = v[0];
+#pragma unroll
+    for (int k = 1; k < NS; ++k) x ^= v[k];
+  }
+  if constexpr (KIND == 0) {
+    // Taken only if four words match a fixed pattern; dst[i] is in bounds.
+    if (x[0] == 0x9e3779b9u && x[1] == 0x7f4a7c15u && x[2] == 0xf39cc060u && x[3] == 0x5ced7e1bu)
+      dst[i] = x;
+  } else {
+    __builtin_nontemporal_store(x, dst + i);
+  }
+}
+
+template <int KIND>
+hipError_t launch_kind(int n_src, const Srcs &s, u32x4 *dst, uint32_t n_vec, hipStream_t st) {
+  const dim3 grid((n_vec + kBlock - 1) / kBlock);
+  switch (n_src) {
+#define CEIL_CASE(N) \
+  case N: hipLaunchKernelGGL((stream_kernel<N, KIND>), grid, dim3(kBlock), 0, st, s, dst, n_vec); break;
+    CEIL_CASE(1) CEIL_CASE(2) CEIL_CASE(3) CEIL_CASE(4) CEIL_CASE(5) CEIL_CASE(6) CEIL_CASE(7)
+    CEIL_CASE(8)
+#undef CEIL_CASE
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace
+
+// Launches one ceiling kernel over n_vec 16-byte vectors on `stream`.
+//   kind   0..3 as above; n_src 1..8 (ignored for kind 3).
+//   src    [n_src] device pointers, 16-byte aligned, n_vec vectors each
+//          (kind 2: src[0] is the interleaved region, n_src * n_vec vectors
+//          rounded up to whole chunks per lane).
+//   dst    device pointer to n_vec vectors (kind 0: written only in the
+//          never-taken case).
+// Returns 0, or -1 for arguments out of range, or the HIP error code of the
+// launch.
+extern "C" __attribute__((visibility("default"))) int ceiling_stream(int kind, const void *const *src,
+                                                                     int n_src, void *dst,
+                                                                     int64_t n_vec, void *stream) {
+  if (kind < 0 || kind > 3 || n_vec < 0 || n_vec >= (int64_t(1) << 31) || !dst) return -1;
+  if (kind != 3 && (n_src < 1 || n_src > 8 || !src)) return -1;
+  if (n_vec == 0) return 0;
+  Srcs s = {};
+  if (kind != 3)
+    for (int k = 0; k < (kind == 2 ? 1 : n_src); ++k) {
+      if (!src[k]) return -1;
+      s.p[k] = static_cast<const u32x4 *>(src[k]);
+    }
+  u32x4 *d = static_cast<u32x4 *>(dst);
+  const uint32_t n = uint32_t(n_vec);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t e;
+  switch (kind) {
+    case 0: e = launch_kind<0>(n_src, s, d, n, st); break;
+    case 1: e = launch_kind<1>(n_src, s, d, n, st); break;
+    case 2: e = launch_kind<2>(n_src, s, d, n, st); break;
+    default: e = launch_kind<3>(1, s, d, n, st); break;
+  }
+  return e == hipSuccess ? 0 : int(e);
+}

@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define CHEB_VERSION 2
+#define CHEB_VERSION 3
 
 #if defined(__GNUC__) || defined(__clang__)
 #define CHEB_API __attribute__((visibility("default")))
@@ -230,6 +230,28 @@ CHEB_API int cheb_cache_layout(int32_t n_slots, int32_t dtype, const int64_t *se
                       int32_t n_segs, int64_t *seg_offset, int64_t *slot_numel,
                       size_t *slot_stride_bytes, size_t *arena_bytes);
 
+/* How the entries of H are laid out in the arena.
+ *   CHEB_LAYOUT_SLOTS        each entry contiguous ("slot"), slots
+ *                            slot_stride_bytes apart: the layout of
+ *                            cheb_cache_create, the only one a fused push
+ *                            (cheb_cache_begin_push) can write into.
+ *   CHEB_LAYOUT_INTERLEAVED  the arena is cut into 32 KiB chunks taken by the
+ *                            entries in turn: chunk c of the entry in lane j
+ *                            sits (c * n_slots + j) chunks past the first
+ *                            64 KiB boundary of the arena.  One prediction
+ *                            then reads a single region of the arena instead
+ *                            of n separate ones, which streams faster on
+ *                            MI355X; entries are filled by cheb_cache_push.
+ * Outputs of the predictions are contiguous in both layouts. */
+enum { CHEB_LAYOUT_SLOTS = 0, CHEB_LAYOUT_INTERLEAVED = 1 };
+
+/* cheb_cache_arena_bytes for either layout (Section 3.3; Algorithm 1, as
+ * cheb_cache_arena_bytes): arena bytes for n_slots entries laid out as
+ * `layout` (the interleaved layout includes room to start on a 64 KiB
+ * boundary).  Errors: CHEB_E_INVAL, CHEB_E_DTYPE. */
+CHEB_API int cheb_cache_arena_bytes_ex(int32_t n_slots, int32_t dtype, const int64_t *seg_numel,
+                                       int32_t n_segs, int32_t layout, size_t *arena_bytes);
+
 /* Creates the history buffer H of Section 3.3 (n = n_slots entries, empty
  * at the start of sampling; Algorithm 1, online stage) over `arena`
  * (device, 256-byte aligned, at least the bytes cheb_cache_arena_bytes
@@ -238,6 +260,23 @@ CHEB_API int cheb_cache_layout(int32_t n_slots, int32_t dtype, const int64_t *se
 CHEB_API int cheb_cache_create(cheb_cache **out, int32_t n_slots, int32_t dtype,
                       const int64_t *seg_numel, int32_t n_segs, void *arena,
                       size_t arena_bytes);
+
+/* cheb_cache_create with a choice of layout (CHEB_LAYOUT_SLOTS, as
+ * cheb_cache_create, or CHEB_LAYOUT_INTERLEAVED); arena_bytes at least
+ * cheb_cache_arena_bytes_ex for that layout.  Errors: as
+ * cheb_cache_create. */
+CHEB_API int cheb_cache_create_ex(cheb_cache **out, int32_t n_slots, int32_t dtype,
+                                  const int64_t *seg_numel, int32_t n_segs, int32_t layout,
+                                  void *arena, size_t arena_bytes);
+
+/* Where the elements of an entry lie: element e of the entry whose base
+ * cheb_cache_entry gives is at
+ *     base + (e / chunk_elems) * entry_stride_elems + e % chunk_elems
+ * elements.  For CHEB_LAYOUT_SLOTS entry_stride_elems == chunk_elems, so
+ * the entry is contiguous.  Every output may be NULL.  Errors:
+ * CHEB_E_INVAL. */
+CHEB_API int cheb_cache_geometry(const cheb_cache *c, int32_t *layout, int64_t *chunk_elems,
+                                 int64_t *entry_stride_elems);
 
 /* Ends the history buffer H of Section 3.3 (Algorithm 1, end of the
  * sampling loop): frees the handle, not the arena.  NULL is accepted. */
@@ -274,8 +313,9 @@ CHEB_API int cheb_cache_push(cheb_cache *c, double t, const void *const *seg_src
  * after each segment keeps whatever the slot held, so the padding elements
  * of later predictions are unspecified (they may be NaN); every segment's
  * own elements are exact.  Until cheb_cache_commit, pushes and
- * extrapolations fail with CHEB_E_NOTREADY.  Errors: CHEB_E_INVAL,
- * CHEB_E_NOTREADY (already open). */
+ * extrapolations fail with CHEB_E_NOTREADY.  Only for CHEB_LAYOUT_SLOTS.
+ * Errors: CHEB_E_INVAL (also for an interleaved cache), CHEB_E_NOTREADY
+ * (already open). */
 CHEB_API int cheb_cache_begin_push(cheb_cache *c, void **slot_base);
 
 /* Fused push, part 2 (Algorithm 1, full computation: store (s, f_s) in H):
@@ -299,8 +339,9 @@ CHEB_API int cheb_cache_abort_push(cheb_cache *c);
 CHEB_API int cheb_cache_history(const cheb_cache *c, double *t_out, int32_t *count);
 
 /* Device address of the features f_{s_j} of held entry j (Section 3.3;
- * Algorithm 1), j = `idx` counted from the oldest (0).  Errors:
- * CHEB_E_INVAL (idx outside 0 .. count-1). */
+ * Algorithm 1), j = `idx` counted from the oldest (0): the entry's first
+ * element; the others follow cheb_cache_geometry.  Errors: CHEB_E_INVAL
+ * (idx outside 0 .. count-1). */
 CHEB_API int cheb_cache_entry(const cheb_cache *c, int32_t idx, void **slot_base);
 
 /* Element offset of cached tensor `seg` (one module output of the block

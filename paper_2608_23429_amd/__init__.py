@@ -13,6 +13,8 @@ import numpy as np
 import torch
 
 from ._binding import (  # noqa: F401  (re-exported C entry points)
+    CHEB_LAYOUT_INTERLEAVED, CHEB_LAYOUT_SLOTS, cheb_cache_arena_bytes_ex, cheb_cache_create_ex,
+    cheb_cache_geometry,
     CHEB_BF16, CHEB_F16, CHEB_F32, CHEB_MAX_NODES, CHEB_MAX_OUTPUTS, CHEB_MAX_SLOTS, CHEB_RHO_ALTERNATING,
     CHEB_RHO_GENERAL, CHEB_SHORT_FULL, CHEB_TAYLOR, CHEB_SHORT_LOWER, ChebError, cheb_chebyshev_nodes,
     cheb_precompute_weights_variant,
@@ -220,33 +222,44 @@ class ResidualHistory:
         self.cache.close()
 
 
+_LAYOUTS = {"slots": CHEB_LAYOUT_SLOTS, "interleaved": CHEB_LAYOUT_INTERLEAVED}
+
+
 class ChebCache:
     """The history ring of one feature set, over a torch-allocated arena.
 
     ``seg_numel`` lists the element counts of the cached tensors in cache
-    order.  Outputs and slots share one flat layout; ``segment_views``
-    cuts a flat buffer into per-segment views.
+    order.  Outputs (and, in the slot layout, entries) share one flat
+    layout; ``segment_views`` cuts a flat buffer into per-segment views.
+    ``layout`` is "slots" (contiguous entries; fused push possible) or
+    "interleaved" (entries cut into 32 KiB chunks taken in turn; filled by
+    ``push``).
     """
 
     def __init__(self, n_slots: int, dtype: torch.dtype, seg_numel: Sequence[int],
-                 device=None, arena: Optional[torch.Tensor] = None):
+                 device=None, arena: Optional[torch.Tensor] = None, layout: str = "slots"):
         self.n_slots = int(n_slots)
         self.dtype = dtype
         self.cdtype = cheb_dtype(dtype)
         self.seg_numel = [int(n) for n in seg_numel]
+        if layout not in _LAYOUTS:
+            raise ChebError(_binding.CHEB_E_INVAL, f"unknown layout {layout!r}")
+        self.layout = layout
         lay = cheb_cache_layout(self.n_slots, self.cdtype, self.seg_numel)
         self.seg_offset = [int(o) for o in lay["seg_offset"]]
         self.slot_numel = int(lay["slot_numel"])
         self.slot_stride_bytes = int(lay["slot_stride_bytes"])
-        self.arena_bytes = int(lay["arena_bytes"])
+        self.arena_bytes = cheb_cache_arena_bytes_ex(self.n_slots, self.cdtype, self.seg_numel,
+                                                     _LAYOUTS[layout])
         if arena is None:
             device = torch.device("cuda", torch.cuda.current_device()) if device is None else device
             arena = torch.empty(self.arena_bytes, dtype=torch.uint8, device=device)
         _check_device_tensor(arena, "arena")
         self.arena = arena
         self.device = arena.device
-        self._h = cheb_cache_create(self.n_slots, self.cdtype, self.seg_numel,
-                                    arena.data_ptr(), arena.numel() * arena.element_size())
+        self._h = cheb_cache_create_ex(self.n_slots, self.cdtype, self.seg_numel, _LAYOUTS[layout],
+                                       arena.data_ptr(), arena.numel() * arena.element_size())
+        _, self.chunk_elems, self.entry_stride_elems = cheb_cache_geometry(self._h)
 
     # -- lifetime ------------------------------------------------------------
     def close(self):
@@ -282,8 +295,22 @@ class ChebCache:
         return raw.view(self.dtype)
 
     def entry(self, idx: int) -> torch.Tensor:
-        """Flat view of the held entry of age index idx (0 = oldest)."""
-        return self._slot_tensor(cheb_cache_entry(self._h, idx))
+        """The held entry of age index idx (0 = oldest) as a flat tensor: a
+        view of its slot in the slot layout, a gathered copy of its chunks
+        in the interleaved layout."""
+        addr = cheb_cache_entry(self._h, idx)
+        if self.layout == "slots":
+            return self._slot_tensor(addr)
+        esz = torch.empty((), dtype=self.dtype).element_size()
+        start = (addr - self.arena.data_ptr()) // esz
+        chunk, stride = self.chunk_elems, self.entry_stride_elems
+        n_chunks = -(-self.slot_numel // chunk)
+        if n_chunks == 0:
+            return torch.empty(0, dtype=self.dtype, device=self.device)
+        whole = self.arena.view(self.dtype)
+        chunks = torch.as_strided(whole, (n_chunks, chunk), (stride, 1),
+                                  storage_offset=whole.storage_offset() + start)
+        return chunks.reshape(-1)[:self.slot_numel].clone()
 
     # -- the online stage ------------------------------------------------------
     def push(self, t: float, segments: Sequence[torch.Tensor],

@@ -30,6 +30,9 @@ CHEB_RHO_GENERAL = 0
 CHEB_RHO_ALTERNATING = 1
 CHEB_TAYLOR = 2
 
+CHEB_LAYOUT_SLOTS = 0
+CHEB_LAYOUT_INTERLEAVED = 1
+
 CHEB_BF16 = 0
 CHEB_F32 = 1
 CHEB_F16 = 2
@@ -78,6 +81,11 @@ SIGNATURES = {
     "cheb_combine_multi": [_vpp, ctypes.c_int32, _dp, ctypes.c_int32, _vpp, ctypes.c_int64,
                            ctypes.c_int32, _vp],
     "cheb_cache_arena_bytes": [ctypes.c_int32, ctypes.c_int32, _i64p, ctypes.c_int32, _szp, _szp],
+    "cheb_cache_arena_bytes_ex": [ctypes.c_int32, ctypes.c_int32, _i64p, ctypes.c_int32,
+                                  ctypes.c_int32, _szp],
+    "cheb_cache_create_ex": [ctypes.POINTER(_vp), ctypes.c_int32, ctypes.c_int32, _i64p,
+                             ctypes.c_int32, ctypes.c_int32, _vp, ctypes.c_size_t],
+    "cheb_cache_geometry": [_vp, _i32p, _i64p, _i64p],
     "cheb_cache_layout": [ctypes.c_int32, ctypes.c_int32, _i64p, ctypes.c_int32, _i64p,
                           _i64p, _szp, _szp],
     "cheb_cache_create": [ctypes.POINTER(_vp), ctypes.c_int32, ctypes.c_int32, _i64p,
@@ -206,6 +214,33 @@ def cheb_cache_arena_bytes(n_slots, dtype, seg_numel):
     _check(LIB.cheb_cache_arena_bytes(int(n_slots), int(dtype), seg.ctypes.data_as(_i64p),
                                       seg.size, ctypes.byref(arena), ctypes.byref(stride)))
     return arena.value, stride.value
+
+
+def cheb_cache_arena_bytes_ex(n_slots, dtype, seg_numel, layout):
+    seg = np.ascontiguousarray(seg_numel, dtype=np.int64).reshape(-1)
+    arena = ctypes.c_size_t()
+    _check(LIB.cheb_cache_arena_bytes_ex(int(n_slots), int(dtype), seg.ctypes.data_as(_i64p),
+                                         seg.size, int(layout), ctypes.byref(arena)))
+    return arena.value
+
+
+def cheb_cache_create_ex(n_slots, dtype, seg_numel, layout, arena_ptr, arena_bytes):
+    seg = np.ascontiguousarray(seg_numel, dtype=np.int64).reshape(-1)
+    h = ctypes.c_void_p()
+    _check(LIB.cheb_cache_create_ex(ctypes.byref(h), int(n_slots), int(dtype),
+                                    seg.ctypes.data_as(_i64p), seg.size, int(layout),
+                                    ctypes.c_void_p(int(arena_ptr)), int(arena_bytes)))
+    return h
+
+
+def cheb_cache_geometry(handle):
+    """(layout, chunk_elems, entry_stride_elems) of a cache."""
+    lay = ctypes.c_int32()
+    chunk = ctypes.c_int64()
+    stride = ctypes.c_int64()
+    _check(LIB.cheb_cache_geometry(handle, ctypes.byref(lay), ctypes.byref(chunk),
+                                   ctypes.byref(stride)))
+    return lay.value, chunk.value, stride.value
 
 
 def cheb_cache_layout(n_slots, dtype, seg_numel):

@@ -332,6 +332,24 @@ int cheb_chebyshev_nodes(int32_t n, int32_t kind, double a, double b, double *x_
 
 int cheb_combine_multi(const void *const *src, int32_t n_src, const double *w, int32_t n_out,
                        void *const *out, int64_t numel, int32_t dtype, void *stream) {
+  return combine_checked(src, n_src, w, n_out, out, numel, dtype, kChunkVecs, stream);
+}
+
+int cheb_combine(const void *const *src, int32_t n_src, const double *w, void *out,
+                 int64_t numel, int32_t dtype, void *stream) {
+  void *outs[1] = {out};
+  if (numel > 0 && !out) return fail(CHEB_E_INVAL, "out is NULL");
+  return cheb_combine_multi(src, n_src, w, 1, outs, numel, dtype, stream);
+}
+
+}  // extern "C"
+
+namespace cheb {
+
+int combine_checked(const void *const *src, int32_t n_src, const double *w, int32_t n_out,
+                    void *const *out, int64_t numel, int32_t dtype, int64_t super_vecs,
+                    void *stream) {
+  const bool contiguous = super_vecs == kChunkVecs;
   if (!valid_dtype(dtype)) return fail(CHEB_E_DTYPE, "unknown dtype %d", dtype);
   if (n_src < 1 || n_src > CHEB_MAX_SLOTS)
     return fail(CHEB_E_INVAL, "n_src %d outside 1..%d", n_src, CHEB_MAX_SLOTS);
@@ -347,6 +365,8 @@ int cheb_combine_multi(const void *const *src, int32_t n_src, const double *w, i
     if (dtype != CHEB_F32 && fabs(w[m]) > double(FLT_MAX))
       return fail(CHEB_E_NONFINITE, "weight %d (%.17g) overflows fp32", m, w[m]);
   }
+  if (!contiguous && numel % elems_per_vec(dtype) != 0)
+    return fail(CHEB_E_INVAL, "interleaved sources need whole 16-byte vectors");
   if (numel == 0) return ok();
   const uintptr_t bytes = uintptr_t(numel) * elem_bytes(dtype);
   auto overlap = [bytes](const void *a, const void *b) {
@@ -360,20 +380,16 @@ int cheb_combine_multi(const void *const *src, int32_t n_src, const double *w, i
   for (int m = 0; m < n_out; ++m) {
     if (!out[m]) return fail(CHEB_E_INVAL, "out[%d] is NULL", m);
     if (!aligned16(out[m])) return fail(CHEB_E_ALIGN, "out[%d] is not 16-byte aligned", m);
-    for (int k = 0; k < n_src; ++k)
-      if (overlap(out[m], src[k])) return fail(CHEB_E_INVAL, "out[%d] overlaps src[%d]", m, k);
+    // Interleaved sources spread over their arena; the cache checks the
+    // outputs against the whole arena instead.
+    if (contiguous)
+      for (int k = 0; k < n_src; ++k)
+        if (overlap(out[m], src[k])) return fail(CHEB_E_INVAL, "out[%d] overlaps src[%d]", m, k);
     for (int j = 0; j < m; ++j)
       if (overlap(out[m], out[j])) return fail(CHEB_E_INVAL, "out[%d] overlaps out[%d]", m, j);
   }
-  return launch_combine(dtype, src, n_src, w, n_out, out, numel,
+  return launch_combine(dtype, src, n_src, w, n_out, out, numel, super_vecs,
                         static_cast<hipStream_t>(stream));
 }
 
-int cheb_combine(const void *const *src, int32_t n_src, const double *w, void *out,
-                 int64_t numel, int32_t dtype, void *stream) {
-  void *outs[1] = {out};
-  if (numel > 0 && !out) return fail(CHEB_E_INVAL, "out is NULL");
-  return cheb_combine_multi(src, n_src, w, 1, outs, numel, dtype, stream);
-}
-
-}  // extern "C"
+}  // namespace cheb

@@ -1,6 +1,7 @@
 // History cache: the fixed-size FIFO of full-step features (paper,
 // Section 3.3, forward application; Algorithm 1, online stage) kept as a
-// ring of slots in one caller-owned device arena.
+// ring of entries in one caller-owned device arena, either as contiguous
+// slots or as chunk-interleaved lanes (internal.h).
 #include <math.h>
 #include <string.h>
 
@@ -20,6 +21,9 @@ struct cheb_cache {
   size_t slot_stride = 0;
   char *arena = nullptr;
   size_t arena_bytes = 0;
+  int32_t layout = CHEB_LAYOUT_SLOTS;
+  char *region = nullptr;          // interleaved: first lane, on a kLaneAlign boundary
+  int64_t super_vecs = kChunkVecs; // chunk stride of an entry (vectors)
   // Ring state: `head` is the slot the next entry goes to; the `count` held
   // entries, oldest first, are in slots head - count, ..., head - 1 (mod n).
   double slot_t[CHEB_MAX_SLOTS] = {0};
@@ -30,7 +34,11 @@ struct cheb_cache {
   int32_t slot_of_age(int32_t age) const {
     return ((head - count + age) % n_slots + n_slots) % n_slots;
   }
-  char *slot_ptr(int32_t slot) const { return arena + size_t(slot) * slot_stride; }
+  // Base of the entry stored in `slot` (its first vector).
+  char *slot_ptr(int32_t slot) const {
+    return layout == CHEB_LAYOUT_SLOTS ? arena + size_t(slot) * slot_stride
+                                       : region + size_t(slot) * kChunkBytes;
+  }
 };
 
 namespace {
@@ -63,6 +71,18 @@ int layout(int32_t n_slots, int32_t dtype, const int64_t *seg_numel, int32_t n_s
 }
 
 bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// Arena bytes of the interleaved layout: every lane padded to whole chunks,
+// plus room to start the region on a kLaneAlign boundary.
+size_t interleaved_bytes(int32_t n_slots, int64_t slot_numel, int dtype) {
+  const int64_t vecs = slot_numel / elems_per_vec(dtype);
+  const int64_t chunks = (vecs + kChunkVecs - 1) / kChunkVecs;
+  return size_t(chunks) * size_t(n_slots) * kChunkBytes + kLaneAlign;
+}
+
+bool valid_layout(int32_t layout) {
+  return layout == CHEB_LAYOUT_SLOTS || layout == CHEB_LAYOUT_INTERLEAVED;
+}
 
 // CHEB_E_DUPNODE when t equals an abscissa that stays held after the next
 // entry goes in (a full ring drops its oldest first).
@@ -102,6 +122,8 @@ int extrapolate_newest(cheb_cache *c, int32_t used, const double *w, int32_t n_o
     return fail(CHEB_E_INVAL, "n_out %d outside 1..%d", n_out, CHEB_MAX_OUTPUTS);
   const void *src[CHEB_MAX_SLOTS];
   for (int32_t j = 0; j < used; ++j) src[j] = c->slot_ptr(c->slot_of_age(c->count - used + j));
+  // Outputs may not touch the arena (for interleaved entries the sources
+  // spread over all of it).
   if (c->slot_numel > 0) {
     const uintptr_t a0 = reinterpret_cast<uintptr_t>(c->arena);
     const uintptr_t ob = uintptr_t(c->slot_numel) * uintptr_t(elem_bytes(c->dtype));
@@ -112,7 +134,8 @@ int extrapolate_newest(cheb_cache *c, int32_t used, const double *w, int32_t n_o
         return fail(CHEB_E_INVAL, "out[%d] overlaps the cache arena", m);
     }
   }
-  return cheb_combine_multi(src, used, w, n_out, out, c->slot_numel, c->dtype, stream);
+  return combine_checked(src, used, w, n_out, out, c->slot_numel, c->dtype, c->super_vecs,
+                         stream);
 }
 
 int cache_view(const cheb_cache *c, CacheView *v) {
@@ -125,6 +148,8 @@ int cache_view(const cheb_cache *c, CacheView *v) {
   v->seg_numel = c->seg_numel.data();
   v->seg_offset = c->seg_offset.data();
   v->slot_numel = c->slot_numel;
+  v->layout = c->layout;
+  v->super_vecs = c->super_vecs;
   v->arena = c->arena;
   v->arena_bytes = c->arena_bytes;
   return CHEB_OK;
@@ -162,15 +187,31 @@ int cheb_cache_layout(int32_t n_slots, int32_t dtype, const int64_t *seg_numel, 
   return ok();
 }
 
-int cheb_cache_create(cheb_cache **out, int32_t n_slots, int32_t dtype, const int64_t *seg_numel,
-                      int32_t n_segs, void *arena, size_t arena_bytes) {
+int cheb_cache_arena_bytes_ex(int32_t n_slots, int32_t dtype, const int64_t *seg_numel,
+                              int32_t n_segs, int32_t layout_kind, size_t *arena_bytes) {
+  if (!arena_bytes) return fail(CHEB_E_INVAL, "arena_bytes is NULL");
+  if (!valid_layout(layout_kind)) return fail(CHEB_E_INVAL, "unknown layout %d", layout_kind);
+  std::vector<int64_t> off;
+  int64_t sn = 0;
+  size_t st = 0, ab = 0;
+  int rc = layout(n_slots, dtype, seg_numel, n_segs, &off, &sn, &st, &ab);
+  if (rc != CHEB_OK) return rc;
+  *arena_bytes = layout_kind == CHEB_LAYOUT_SLOTS ? ab : interleaved_bytes(n_slots, sn, dtype);
+  return ok();
+}
+
+int cheb_cache_create_ex(cheb_cache **out, int32_t n_slots, int32_t dtype,
+                         const int64_t *seg_numel, int32_t n_segs, int32_t layout_kind,
+                         void *arena, size_t arena_bytes) {
   if (!out) return fail(CHEB_E_INVAL, "out is NULL");
   *out = nullptr;
+  if (!valid_layout(layout_kind)) return fail(CHEB_E_INVAL, "unknown layout %d", layout_kind);
   std::vector<int64_t> off;
   int64_t sn = 0;
   size_t st = 0, need = 0;
   int rc = layout(n_slots, dtype, seg_numel, n_segs, &off, &sn, &st, &need);
   if (rc != CHEB_OK) return rc;
+  if (layout_kind == CHEB_LAYOUT_INTERLEAVED) need = interleaved_bytes(n_slots, sn, dtype);
   if (!arena) return fail(CHEB_E_INVAL, "arena is NULL");
   if (!aligned(arena, kSlotAlign)) return fail(CHEB_E_ALIGN, "arena is not 256-byte aligned");
   if (arena_bytes < need)
@@ -185,7 +226,29 @@ int cheb_cache_create(cheb_cache **out, int32_t n_slots, int32_t dtype, const in
   c->slot_stride = st;
   c->arena = static_cast<char *>(arena);
   c->arena_bytes = arena_bytes;
+  c->layout = layout_kind;
+  if (layout_kind == CHEB_LAYOUT_INTERLEAVED) {
+    const uintptr_t a = reinterpret_cast<uintptr_t>(arena);
+    c->region = reinterpret_cast<char *>((a + kLaneAlign - 1) / kLaneAlign * kLaneAlign);
+    c->super_vecs = int64_t(n_slots) * kChunkVecs;
+  }
   *out = c;
+  return ok();
+}
+
+int cheb_cache_create(cheb_cache **out, int32_t n_slots, int32_t dtype, const int64_t *seg_numel,
+                      int32_t n_segs, void *arena, size_t arena_bytes) {
+  return cheb_cache_create_ex(out, n_slots, dtype, seg_numel, n_segs, CHEB_LAYOUT_SLOTS, arena,
+                              arena_bytes);
+}
+
+int cheb_cache_geometry(const cheb_cache *c, int32_t *layout_kind, int64_t *chunk_elems,
+                        int64_t *entry_stride_elems) {
+  if (!c) return fail(CHEB_E_INVAL, "cache is NULL");
+  const int64_t vec = elems_per_vec(c->dtype);
+  if (layout_kind) *layout_kind = c->layout;
+  if (chunk_elems) *chunk_elems = kChunkVecs * vec;
+  if (entry_stride_elems) *entry_stride_elems = c->super_vecs * vec;
   return ok();
 }
 
@@ -223,7 +286,7 @@ int cheb_cache_push(cheb_cache *c, double t, const void *const *seg_src, void *s
   // first launch, so a launch that fails after an earlier one has written
   // part of the slot cannot leave a half-overwritten entry in the history.
   const int32_t slot = claim_slot(c);
-  rc = launch_gather(c->dtype, c->slot_ptr(slot), segs.data(), int(n_segs),
+  rc = launch_gather(c->dtype, c->slot_ptr(slot), segs.data(), int(n_segs), c->super_vecs,
                      static_cast<hipStream_t>(stream));
   if (rc != CHEB_OK) return rc;
   record(c, t);
@@ -232,6 +295,8 @@ int cheb_cache_push(cheb_cache *c, double t, const void *const *seg_src, void *s
 
 int cheb_cache_begin_push(cheb_cache *c, void **slot_base) {
   if (!c || !slot_base) return fail(CHEB_E_INVAL, "cache or slot_base is NULL");
+  if (c->layout != CHEB_LAYOUT_SLOTS)
+    return fail(CHEB_E_INVAL, "a fused push needs contiguous slots (CHEB_LAYOUT_SLOTS)");
   if (c->push_open) return fail(CHEB_E_NOTREADY, "a fused push is already open");
   const int32_t slot = claim_slot(c);
   c->push_open = true;

@@ -18,6 +18,11 @@
 // 3. Residual application on a skipped step (Section 3.1, block equation):
 //    the block stack's sum of predicted module outputs added to the
 //    residual stream in one pass.
+// History entries are either contiguous slots or chunk-interleaved lanes
+// (internal.h): vector v of an entry is at (v / 2048) * super + v % 2048
+// from the entry's base, which is v itself when super is 2048.  Every
+// kernel tests that one uniform value and takes the plain 32-bit indexing
+// for contiguous entries.
 #include <hip/hip_runtime.h>
 
 #include <stdint.h>
@@ -49,12 +54,19 @@ __device__ __forceinline__ void store16(u32x4 *p, u32x4 v) {
 
 // History pointers (oldest to newest), output pointers and one weight row
 // per output, passed by value as kernel arguments (they land in SGPRs).
+// `super` is the entries' chunk stride in vectors (kChunkVecs: contiguous).
 template <int NS, int NO, typename W>
 struct Hist {
   const u32x4 *p[NS];
   u32x4 *o[NO];
   W w[NO][NS];
+  uint64_t super;
 };
+
+// Vector v of an interleaved entry, relative to the entry's base.
+__device__ __forceinline__ uint64_t lane_vec(uint64_t v, uint64_t super) {
+  return (v >> kChunkShift) * super + (v & uint64_t(kChunkVecs - 1));
+}
 
 // Ragged end of a stateless combination: `count` (< elements per vector)
 // trailing elements starting at element `first`, done by block 0.
@@ -204,14 +216,24 @@ template <class Op, int NS, int NO, int BLK, int U, bool NT>
 __global__ __launch_bounds__(BLK) void combine_kernel(Hist<NS, NO, typename Op::W> h,
                                                       uint32_t n_vec, uint32_t n_tiles,
                                                       Tail tail) {
+  const bool flat = h.super == uint64_t(kChunkVecs);
   for (uint32_t tile = blockIdx.x; tile < n_tiles; tile += gridDim.x) {
     const uint32_t base = tile * uint32_t(BLK * U) + threadIdx.x;
     if (base + uint32_t((U - 1) * BLK) < n_vec) {
       u32x4 v[U][NS];
+      if (flat) {
 #pragma unroll
-      for (int u = 0; u < U; ++u)
+        for (int u = 0; u < U; ++u)
 #pragma unroll
-        for (int k = 0; k < NS; ++k) v[u][k] = load16<NT>(h.p[k] + base + u * BLK);
+          for (int k = 0; k < NS; ++k) v[u][k] = load16<NT>(h.p[k] + base + u * BLK);
+      } else {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const uint64_t off = lane_vec(base + u * BLK, h.super);
+#pragma unroll
+          for (int k = 0; k < NS; ++k) v[u][k] = load16<NT>(h.p[k] + off);
+        }
+      }
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int u = 0; u < U; ++u)
@@ -223,15 +245,17 @@ __global__ __launch_bounds__(BLK) void combine_kernel(Hist<NS, NO, typename Op::
       for (int u = 0; u < U; ++u) {
         const uint32_t i = base + u * BLK;
         if (i < n_vec) {
+          const uint64_t off = flat ? uint64_t(i) : lane_vec(i, h.super);
           u32x4 v[NS];
 #pragma unroll
-          for (int k = 0; k < NS; ++k) v[k] = load16<NT>(h.p[k] + i);
+          for (int k = 0; k < NS; ++k) v[k] = load16<NT>(h.p[k] + off);
 #pragma unroll
           for (int m = 0; m < NO; ++m) store16<NT>(h.o[m] + i, Op::template vec<NS>(v, h.w[m]));
         }
       }
     }
   }
+  // A ragged tail only exists for contiguous sources (the host ensures it).
   if (tail.count != 0 && blockIdx.x == 0 && threadIdx.x < tail.count) {
     using E = typename Op::E;
     const E *p[NS];
@@ -287,9 +311,11 @@ hipError_t launch_many(const Hist<NS, NO, typename Op::W> &h, uint32_t n_vec, Ta
 
 template <class Op, int NS, int NO>
 hipError_t launch_ns_no(const void *const *src, const double *w, void *const *out,
-                        int64_t numel, const cheb_launch_config &cfg, int cus, hipStream_t s) {
+                        int64_t numel, int64_t super_vecs, const cheb_launch_config &cfg, int cus,
+                        hipStream_t s) {
   constexpr int kVec = 16 / int(sizeof(typename Op::E));
   Hist<NS, NO, typename Op::W> h;
+  h.super = uint64_t(super_vecs);
   for (int k = 0; k < NS; ++k) h.p[k] = static_cast<const u32x4 *>(src[k]);
   for (int m = 0; m < NO; ++m) {
     h.o[m] = static_cast<u32x4 *>(out[m]);
@@ -307,32 +333,33 @@ hipError_t launch_ns_no(const void *const *src, const double *w, void *const *ou
 
 template <class Op, int NS>
 hipError_t launch_ns(const void *const *src, const double *w, int n_out, void *const *out,
-                     int64_t numel, const cheb_launch_config &cfg, int cus, hipStream_t s) {
+                     int64_t numel, int64_t sv, const cheb_launch_config &cfg, int cus,
+                     hipStream_t s) {
   switch (n_out) {
-    case 1: return launch_ns_no<Op, NS, 1>(src, w, out, numel, cfg, cus, s);
-    case 2: return launch_ns_no<Op, NS, 2>(src, w, out, numel, cfg, cus, s);
-    case 3: return launch_ns_no<Op, NS, 3>(src, w, out, numel, cfg, cus, s);
-    case 4: return launch_ns_no<Op, NS, 4>(src, w, out, numel, cfg, cus, s);
-    case 5: return launch_ns_no<Op, NS, 5>(src, w, out, numel, cfg, cus, s);
-    case 6: return launch_ns_no<Op, NS, 6>(src, w, out, numel, cfg, cus, s);
-    case 7: return launch_ns_no<Op, NS, 7>(src, w, out, numel, cfg, cus, s);
-    default: return launch_ns_no<Op, NS, 8>(src, w, out, numel, cfg, cus, s);
+    case 1: return launch_ns_no<Op, NS, 1>(src, w, out, numel, sv, cfg, cus, s);
+    case 2: return launch_ns_no<Op, NS, 2>(src, w, out, numel, sv, cfg, cus, s);
+    case 3: return launch_ns_no<Op, NS, 3>(src, w, out, numel, sv, cfg, cus, s);
+    case 4: return launch_ns_no<Op, NS, 4>(src, w, out, numel, sv, cfg, cus, s);
+    case 5: return launch_ns_no<Op, NS, 5>(src, w, out, numel, sv, cfg, cus, s);
+    case 6: return launch_ns_no<Op, NS, 6>(src, w, out, numel, sv, cfg, cus, s);
+    case 7: return launch_ns_no<Op, NS, 7>(src, w, out, numel, sv, cfg, cus, s);
+    default: return launch_ns_no<Op, NS, 8>(src, w, out, numel, sv, cfg, cus, s);
   }
 }
 
 template <class Op>
 hipError_t launch_op(const void *const *src, int n, const double *w, int n_out,
-                     void *const *out, int64_t numel, const cheb_launch_config &cfg, int cus,
-                     hipStream_t s) {
+                     void *const *out, int64_t numel, int64_t sv,
+                     const cheb_launch_config &cfg, int cus, hipStream_t s) {
   switch (n) {
-    case 1: return launch_ns<Op, 1>(src, w, n_out, out, numel, cfg, cus, s);
-    case 2: return launch_ns<Op, 2>(src, w, n_out, out, numel, cfg, cus, s);
-    case 3: return launch_ns<Op, 3>(src, w, n_out, out, numel, cfg, cus, s);
-    case 4: return launch_ns<Op, 4>(src, w, n_out, out, numel, cfg, cus, s);
-    case 5: return launch_ns<Op, 5>(src, w, n_out, out, numel, cfg, cus, s);
-    case 6: return launch_ns<Op, 6>(src, w, n_out, out, numel, cfg, cus, s);
-    case 7: return launch_ns<Op, 7>(src, w, n_out, out, numel, cfg, cus, s);
-    default: return launch_ns<Op, 8>(src, w, n_out, out, numel, cfg, cus, s);
+    case 1: return launch_ns<Op, 1>(src, w, n_out, out, numel, sv, cfg, cus, s);
+    case 2: return launch_ns<Op, 2>(src, w, n_out, out, numel, sv, cfg, cus, s);
+    case 3: return launch_ns<Op, 3>(src, w, n_out, out, numel, sv, cfg, cus, s);
+    case 4: return launch_ns<Op, 4>(src, w, n_out, out, numel, sv, cfg, cus, s);
+    case 5: return launch_ns<Op, 5>(src, w, n_out, out, numel, sv, cfg, cus, s);
+    case 6: return launch_ns<Op, 6>(src, w, n_out, out, numel, sv, cfg, cus, s);
+    case 7: return launch_ns<Op, 7>(src, w, n_out, out, numel, sv, cfg, cus, s);
+    default: return launch_ns<Op, 8>(src, w, n_out, out, numel, sv, cfg, cus, s);
   }
 }
 
@@ -352,9 +379,12 @@ struct GatherArgs {
 // Grid: x = 1024-vector chunk within a segment, y = segment.  Blocks past
 // their segment's end return at once, so no block searches for its
 // segment.  Source reads and slot writes are streaming (each byte is touched
-// once per push), so both carry the non-temporal hint.
+// once per push), so both carry the non-temporal hint.  Vector v of the
+// entry goes v vectors past `slot` (contiguous entry) or to its chunk
+// position in an interleaved lane.
 template <typename E>
-__global__ __launch_bounds__(kGatherBlock) void gather_kernel(GatherArgs a, char *__restrict__ slot) {
+__global__ __launch_bounds__(kGatherBlock) void gather_kernel(GatherArgs a, char *__restrict__ slot,
+                                                              uint64_t super) {
   constexpr int kVec = 16 / int(sizeof(E));
   const int s = int(blockIdx.y);
   const uint64_t numel = a.numel[s];
@@ -363,10 +393,11 @@ __global__ __launch_bounds__(kGatherBlock) void gather_kernel(GatherArgs a, char
   const uint64_t i = uint64_t(blockIdx.x) * kGatherChunk + threadIdx.x;
   if (i > n_full || (i == n_full && rem == 0)) return;
   const u32x4 *src = static_cast<const u32x4 *>(a.src[s]);
-  E *dst_e = reinterpret_cast<E *>(slot) + a.dst_offset[s];
-  u32x4 *dst = reinterpret_cast<u32x4 *>(dst_e);
+  const uint64_t v = a.dst_offset[s] / kVec + i;  // segment offsets are whole vectors
+  u32x4 *dst = reinterpret_cast<u32x4 *>(slot) +
+               (super == uint64_t(kChunkVecs) ? v : lane_vec(v, super));
   if (i < n_full) {
-    store16<true>(dst + i, load16<true>(src + i));
+    store16<true>(dst, load16<true>(src + i));
   } else {
     // Last, partial vector: copy the remaining elements one by one and zero
     // the padding up to the 16-byte boundary.
@@ -376,7 +407,7 @@ __global__ __launch_bounds__(kGatherBlock) void gather_kernel(GatherArgs a, char
     for (int e = 0; e < kVec; ++e) tmp[e] = (uint32_t(e) < rem) ? src_e[n_full * kVec + e] : E(0);
     u32x4 packed;
     memcpy(&packed, tmp, 16);
-    dst[i] = packed;
+    *dst = packed;
   }
 }
 
@@ -432,13 +463,23 @@ template <int NS>
 struct ResArgs {
   uint64_t base[NS];
   double w[NS];
-  int64_t delta[kResCover];
+  int64_t delta[kResCover];  // bytes (contiguous entries) or vectors (interleaved)
   const float *x_in;  // may be null: zero
   float *x_out;
+  uint64_t super;
   uint32_t vec_begin;
   uint32_t n_vec;
   int32_t ncover;
 };
+
+// Source vector of residual vector j in covering segment s of the entry at
+// `base`.
+template <int NS>
+__device__ __forceinline__ const u32x4 *res_src(const ResArgs<NS> &a, bool flat, uint64_t base,
+                                                int32_t s, uint64_t j) {
+  if (flat) return reinterpret_cast<const u32x4 *>(base + uint64_t(a.delta[s]) + j * 16u);
+  return reinterpret_cast<const u32x4 *>(base) + lane_vec(uint64_t(a.delta[s]) + j, a.super);
+}
 
 // Each block starts its walk over the covering segments at a different
 // segment (its index times two, modulo the count), so at any moment the
@@ -464,7 +505,7 @@ __global__ __launch_bounds__(kResBlock) void residual_kernel(ResArgs<NS> a) {
 #pragma unroll
     for (int e = 0; e < V; ++e) acc[e] = 0.0;
   }
-  const uint64_t off = j * 16u;
+  const bool flat = a.super == uint64_t(kChunkVecs);
   const int32_t nc = a.ncover;
   const int32_t start = nc > 0 ? int32_t((uint64_t(blockIdx.x) * 2u) % uint32_t(nc)) : 0;
   int32_t c = 0;
@@ -475,10 +516,8 @@ __global__ __launch_bounds__(kResBlock) void residual_kernel(ResArgs<NS> a) {
     u32x4 v0[NS], v1[NS];
 #pragma unroll
     for (int k = 0; k < NS; ++k) {
-      v0[k] = __builtin_nontemporal_load(
-          reinterpret_cast<const u32x4 *>(a.base[k] + uint64_t(a.delta[s0]) + off));
-      v1[k] = __builtin_nontemporal_load(
-          reinterpret_cast<const u32x4 *>(a.base[k] + uint64_t(a.delta[s1]) + off));
+      v0[k] = __builtin_nontemporal_load(res_src(a, flat, a.base[k], s0, j));
+      v1[k] = __builtin_nontemporal_load(res_src(a, flat, a.base[k], s1, j));
     }
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
@@ -492,9 +531,7 @@ __global__ __launch_bounds__(kResBlock) void residual_kernel(ResArgs<NS> a) {
     if (s0 >= nc) s0 -= nc;
     u32x4 v0[NS];
 #pragma unroll
-    for (int k = 0; k < NS; ++k)
-      v0[k] = __builtin_nontemporal_load(
-          reinterpret_cast<const u32x4 *>(a.base[k] + uint64_t(a.delta[s0]) + off));
+    for (int k = 0; k < NS; ++k) v0[k] = __builtin_nontemporal_load(res_src(a, flat, a.base[k], s0, j));
 #pragma unroll
     for (int k = 0; k < NS; ++k) Dec::add(acc, v0[k], a.w[k]);
   }
@@ -511,9 +548,10 @@ __global__ __launch_bounds__(kResBlock) void residual_kernel(ResArgs<NS> a) {
 template <class Dec, int NS>
 hipError_t launch_residual_ns(const uint64_t *base, const double *w, const int64_t *delta,
                               int ncover, const float *x_in, float *x_out, uint32_t vec_begin,
-                              uint32_t n_vec, hipStream_t s) {
+                              uint32_t n_vec, uint64_t super, hipStream_t s) {
   ResArgs<NS> a;
   memset(&a, 0, sizeof a);
+  a.super = super;
   for (int k = 0; k < NS; ++k) {
     a.base[k] = base[k];
     a.w[k] = w[k];
@@ -532,21 +570,21 @@ hipError_t launch_residual_ns(const uint64_t *base, const double *w, const int64
 template <class Dec>
 hipError_t launch_residual_dec(int n, const uint64_t *base, const double *w, const int64_t *delta,
                                int ncover, const float *x_in, float *x_out, uint32_t vec_begin,
-                               uint32_t n_vec, hipStream_t s) {
+                               uint32_t n_vec, uint64_t sv, hipStream_t s) {
   switch (n) {
 #define CHEB_RES_CASE(N) \
-  case N: return launch_residual_ns<Dec, N>(base, w, delta, ncover, x_in, x_out, vec_begin, n_vec, s);
+  case N: return launch_residual_ns<Dec, N>(base, w, delta, ncover, x_in, x_out, vec_begin, n_vec, sv, s);
     CHEB_RES_CASE(1) CHEB_RES_CASE(2) CHEB_RES_CASE(3) CHEB_RES_CASE(4)
     CHEB_RES_CASE(5) CHEB_RES_CASE(6) CHEB_RES_CASE(7)
 #undef CHEB_RES_CASE
-    default: return launch_residual_ns<Dec, 8>(base, w, delta, ncover, x_in, x_out, vec_begin, n_vec, s);
+    default: return launch_residual_ns<Dec, 8>(base, w, delta, ncover, x_in, x_out, vec_begin, n_vec, sv, s);
   }
 }
 
 }  // namespace
 
 int launch_combine(int dtype, const void *const *src, int n, const double *w, int n_out,
-                   void *const *out, int64_t numel, hipStream_t stream) {
+                   void *const *out, int64_t numel, int64_t super_vecs, hipStream_t stream) {
   if (numel == 0) return ok();
   int cus = 0;
   int rc = device_cus(&cus);
@@ -554,16 +592,22 @@ int launch_combine(int dtype, const void *const *src, int n, const double *w, in
   const cheb_launch_config cfg = launch_shape();
   hipError_t e;
   switch (dtype) {
-    case CHEB_BF16: e = launch_op<Bf16Op>(src, n, w, n_out, out, numel, cfg, cus, stream); break;
-    case CHEB_F16: e = launch_op<F16Op>(src, n, w, n_out, out, numel, cfg, cus, stream); break;
-    default: e = launch_op<F32Op>(src, n, w, n_out, out, numel, cfg, cus, stream); break;
+    case CHEB_BF16:
+      e = launch_op<Bf16Op>(src, n, w, n_out, out, numel, super_vecs, cfg, cus, stream);
+      break;
+    case CHEB_F16:
+      e = launch_op<F16Op>(src, n, w, n_out, out, numel, super_vecs, cfg, cus, stream);
+      break;
+    default:
+      e = launch_op<F32Op>(src, n, w, n_out, out, numel, super_vecs, cfg, cus, stream);
+      break;
   }
   if (e != hipSuccess) return fail(CHEB_E_HIP, "combine launch failed: %s", hipGetErrorString(e));
   return ok();
 }
 
 int launch_gather(int dtype, void *slot_base, const GatherSeg *segs, int n_segs,
-                  hipStream_t stream) {
+                  int64_t super_vecs, hipStream_t stream) {
   const int vec = elems_per_vec(dtype);
   for (int first = 0; first < n_segs; first += kGatherMax) {
     const int count = std::min(kGatherMax, n_segs - first);
@@ -586,10 +630,11 @@ int launch_gather(int dtype, void *slot_base, const GatherSeg *segs, int n_segs,
     a.n = used;
     char *slot = static_cast<char *>(slot_base);
     const dim3 grid{static_cast<uint32_t>(max_chunks), static_cast<uint32_t>(used), 1u};
+    const uint64_t sv = uint64_t(super_vecs);
     if (elem_bytes(dtype) == 2)
-      hipLaunchKernelGGL(gather_kernel<uint16_t>, grid, dim3(kGatherBlock), 0, stream, a, slot);
+      hipLaunchKernelGGL(gather_kernel<uint16_t>, grid, dim3(kGatherBlock), 0, stream, a, slot, sv);
     else
-      hipLaunchKernelGGL(gather_kernel<float>, grid, dim3(kGatherBlock), 0, stream, a, slot);
+      hipLaunchKernelGGL(gather_kernel<float>, grid, dim3(kGatherBlock), 0, stream, a, slot, sv);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return fail(CHEB_E_HIP, "push launch failed: %s", hipGetErrorString(e));
   }
@@ -604,19 +649,20 @@ int residual_max_cover() { return kResCover; }
 
 int launch_residual(int dtype, int n, const uint64_t *base, const double *w, const int64_t *delta,
                     int ncover, const float *x_in, float *x_out, int64_t vec_begin,
-                    int64_t n_vec, hipStream_t stream) {
+                    int64_t n_vec, int64_t super_vecs, hipStream_t stream) {
   if (n_vec == 0) return ok();
   const uint32_t vb = uint32_t(vec_begin), nv = uint32_t(n_vec);
+  const uint64_t sv = uint64_t(super_vecs);
   hipError_t e;
   switch (dtype) {
     case CHEB_BF16:
-      e = launch_residual_dec<Bf16Dec>(n, base, w, delta, ncover, x_in, x_out, vb, nv, stream);
+      e = launch_residual_dec<Bf16Dec>(n, base, w, delta, ncover, x_in, x_out, vb, nv, sv, stream);
       break;
     case CHEB_F16:
-      e = launch_residual_dec<F16Dec>(n, base, w, delta, ncover, x_in, x_out, vb, nv, stream);
+      e = launch_residual_dec<F16Dec>(n, base, w, delta, ncover, x_in, x_out, vb, nv, sv, stream);
       break;
     default:
-      e = launch_residual_dec<F32Dec>(n, base, w, delta, ncover, x_in, x_out, vb, nv, stream);
+      e = launch_residual_dec<F32Dec>(n, base, w, delta, ncover, x_in, x_out, vb, nv, sv, stream);
       break;
   }
   if (e != hipSuccess) return fail(CHEB_E_HIP, "residual launch failed: %s", hipGetErrorString(e));

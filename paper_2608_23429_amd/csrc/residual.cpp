@@ -76,7 +76,7 @@ int check_residual_buffers(const float *x_in, float *x_out, int64_t res_numel) {
 template <class DeltaFn>
 int run(int dtype, int n, const uint64_t *base, const double *w,
         const std::vector<Interval> &plan_iv, DeltaFn delta_of, const float *x_in, float *x_out,
-        hipStream_t stream) {
+        int64_t super_vecs, hipStream_t stream) {
   const int vec = elems_per_vec(dtype);
   const int max_cover = residual_max_cover();
   std::vector<int64_t> delta;
@@ -89,7 +89,7 @@ int run(int dtype, int n, const uint64_t *base, const double *w,
       for (size_t c = 0; c < count; ++c) delta[c] = delta_of(iv.segs[first + c]);
       const float *in = first == 0 ? x_in : x_out;
       int rc = launch_residual(dtype, n, base, w, delta.data(), int(count), in, x_out, vb, nv,
-                               stream);
+                               super_vecs, stream);
       if (rc != CHEB_OK) return rc;
       first += count;
     } while (first < iv.segs.size());
@@ -127,9 +127,16 @@ int cheb_residual_apply(cheb_cache *c, const double *w, const int64_t *res_offse
     if (rc != CHEB_OK) return rc;
     base[k] = reinterpret_cast<uint64_t>(p);
   }
-  const int64_t esize = elem_bytes(v.dtype);
-  auto delta_of = [&](int32_t s) { return (v.seg_offset[s] - res_offset[s]) * esize; };
-  return run(v.dtype, v.n_slots, base, w, iv, delta_of, x_in, x_out,
+  // Contiguous entries: byte offset from the entry base to the segment's
+  // element of residual element 0; interleaved: the same in vectors (the
+  // kernel places each vector by its chunk).
+  const int64_t esize = elem_bytes(v.dtype), vec = elems_per_vec(v.dtype);
+  const bool contiguous = v.super_vecs == kChunkVecs;
+  auto delta_of = [&](int32_t s) {
+    const int64_t d = v.seg_offset[s] - res_offset[s];
+    return contiguous ? d * esize : d / vec;
+  };
+  return run(v.dtype, v.n_slots, base, w, iv, delta_of, x_in, x_out, v.super_vecs,
              static_cast<hipStream_t>(stream));
 }
 
@@ -156,7 +163,8 @@ int cheb_residual_reduce(const void *const *seg_src, const int64_t *seg_numel,
   auto delta_of = [&](int32_t s) {
     return int64_t(reinterpret_cast<uintptr_t>(seg_src[s])) - res_offset[s] * esize;
   };
-  return run(dtype, 1, base, one, iv, delta_of, x_in, x_out, static_cast<hipStream_t>(stream));
+  return run(dtype, 1, base, one, iv, delta_of, x_in, x_out, kChunkVecs,
+             static_cast<hipStream_t>(stream));
 }
 
 }  // extern "C"

@@ -19,11 +19,11 @@ extern "C" void stub_gather_batches_ok(int n) { g_gather_batches_ok.store(n); }
 namespace cheb {
 
 int launch_combine(int, const void *const *, int, const double *, int, void *const *, int64_t,
-                   hipStream_t) {
+                   int64_t, hipStream_t) {
   return fail(CHEB_E_HIP, "host-only build: no device launch");
 }
 
-int launch_gather(int, void *, const GatherSeg *, int n_segs, hipStream_t) {
+int launch_gather(int, void *, const GatherSeg *, int n_segs, int64_t, hipStream_t) {
   for (int first = 0; first < n_segs; first += 64) {
     if (g_gather_batches_ok.fetch_sub(1) <= 0) {
       g_gather_batches_ok.store(0);
@@ -36,7 +36,7 @@ int launch_gather(int, void *, const GatherSeg *, int n_segs, hipStream_t) {
 int residual_max_cover() { return 128; }
 
 int launch_residual(int, int, const uint64_t *, const double *, const int64_t *, int,
-                    const float *, float *, int64_t, int64_t, hipStream_t) {
+                    const float *, float *, int64_t, int64_t, int64_t, hipStream_t) {
   return fail(CHEB_E_HIP, "host-only build: no device launch");
 }
 

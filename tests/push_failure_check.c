@@ -91,6 +91,40 @@ int main(void) {
   CHECK(cheb_cache_history(c, held, &count) == CHEB_OK && count == 3 && held[2] == 3.0);
 
   CHECK(cheb_cache_destroy(c) == CHEB_OK);
+
+  /* The same ring in the interleaved layout over an arena that is 256-byte
+   * but not 64 KiB aligned: the lanes start at the next 64 KiB boundary,
+   * 32 KiB apart, entry j of the ring in lane j mod 6; a failed push drops
+   * the oldest entry as above. */
+  CHECK(cheb_cache_arena_bytes_ex(6, CHEB_BF16, seg, 76, CHEB_LAYOUT_INTERLEAVED, &arena) ==
+        CHEB_OK);
+  const uint64_t chunks = (806879232ULL / 8 + 2047) / 2048;
+  CHECK(arena == chunks * 6 * 32768 + 65536);
+  char *ibase = (char *)(uintptr_t)(((uint64_t)1 << 44) + 256);
+  char *region = (char *)(uintptr_t)(((uint64_t)1 << 44) + 65536);
+  CHECK(cheb_cache_create_ex(&c, 6, CHEB_BF16, seg, 76, CHEB_LAYOUT_INTERLEAVED, ibase,
+                             arena - 1) == CHEB_E_MISMATCH);
+  CHECK(cheb_cache_create_ex(&c, 6, CHEB_BF16, seg, 76, CHEB_LAYOUT_INTERLEAVED, ibase, arena) ==
+        CHEB_OK);
+  int32_t lay = -1;
+  int64_t chunk_elems = 0, lane_stride = 0;
+  CHECK(cheb_cache_geometry(c, &lay, &chunk_elems, &lane_stride) == CHEB_OK);
+  CHECK(lay == CHEB_LAYOUT_INTERLEAVED && chunk_elems == 16384 && lane_stride == 6 * 16384);
+  void *slot_base = NULL;
+  CHECK(cheb_cache_begin_push(c, &slot_base) == CHEB_E_INVAL);
+  stub_gather_batches_ok(2 * 8);
+  for (int i = 0; i < 8; ++i) CHECK(cheb_cache_push(c, 5.0 * i, src, NULL) == CHEB_OK);
+  CHECK(cheb_cache_history(c, held, &count) == CHEB_OK && count == 6 && held[0] == 10.0);
+  for (int a = 0; a < 6; ++a) {
+    void *p = NULL;
+    CHECK(cheb_cache_entry(c, a, &p) == CHEB_OK);
+    CHECK(p == region + 32768 * ((a + 2) % 6));
+  }
+  stub_gather_batches_ok(1);
+  CHECK(cheb_cache_push(c, 40.0, src, NULL) == CHEB_E_HIP);
+  CHECK(cheb_cache_history(c, held, &count) == CHEB_OK && count == 5 && held[0] == 15.0);
+  CHECK(cheb_extrapolate(c, w, out, NULL) == CHEB_E_NOTREADY);
+  CHECK(cheb_cache_destroy(c) == CHEB_OK);
   printf("push failure ok\n");
   return 0;
 }

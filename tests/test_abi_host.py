@@ -47,7 +47,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_version():
-    assert cheb.cheb_version() == 2
+    assert cheb.cheb_version() == 3
 
 
 def _wtol(w, factor=8.0):
@@ -433,3 +433,54 @@ def test_extrapolate_multi_not_ready_and_limits():
         cheb.cheb_extrapolate_at_multi(h, [float("nan")], outs[:1])
     assert e.value.code == B.CHEB_E_NONFINITE
     cheb.cheb_cache_destroy(h)
+
+
+# --------------------------------------------------------------------------
+# Interleaved layout (host side: sizes, geometry, what it refuses)
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype,esize", [(B.CHEB_BF16, 2), (B.CHEB_F16, 2), (B.CHEB_F32, 4)])
+def test_interleaved_arena_bytes(dtype, esize):
+    seg = [1, 8, 13, 0, 1000003, 3, 4096 * 3072]
+    _, pos, stride, arena = _expected_layout(5, esize, seg)
+    assert cheb.cheb_cache_arena_bytes_ex(5, dtype, seg, B.CHEB_LAYOUT_SLOTS) == arena
+    vecs = pos * esize // 16
+    chunks = -(-vecs // 2048)
+    assert cheb.cheb_cache_arena_bytes_ex(5, dtype, seg, B.CHEB_LAYOUT_INTERLEAVED) == \
+        chunks * 5 * 32768 + 65536
+    with pytest.raises(cheb.ChebError) as e:
+        cheb.cheb_cache_arena_bytes_ex(5, dtype, seg, 2)
+    assert e.value.code == B.CHEB_E_INVAL
+
+
+def test_interleaved_create_geometry_and_refusals():
+    seg = [40000, 24, 1 << 20]
+    need = cheb.cheb_cache_arena_bytes_ex(6, B.CHEB_BF16, seg, B.CHEB_LAYOUT_INTERLEAVED)
+    arena = FAKE_ARENA + 256          # 256-byte aligned, not on a 64 KiB boundary
+    with pytest.raises(cheb.ChebError) as e:
+        cheb.cheb_cache_create_ex(6, B.CHEB_BF16, seg, B.CHEB_LAYOUT_INTERLEAVED, arena, need - 1)
+    assert e.value.code == B.CHEB_E_MISMATCH
+    with pytest.raises(cheb.ChebError) as e:
+        cheb.cheb_cache_create_ex(6, B.CHEB_BF16, seg, 7, arena, need)
+    assert e.value.code == B.CHEB_E_INVAL
+    with pytest.raises(cheb.ChebError) as e:
+        cheb.cheb_cache_create_ex(6, B.CHEB_BF16, seg, B.CHEB_LAYOUT_INTERLEAVED, arena + 16, need)
+    assert e.value.code == B.CHEB_E_ALIGN
+    h = cheb.cheb_cache_create_ex(6, B.CHEB_BF16, seg, B.CHEB_LAYOUT_INTERLEAVED, arena, need)
+    try:
+        assert cheb.cheb_cache_geometry(h) == (B.CHEB_LAYOUT_INTERLEAVED, 16384, 6 * 16384)
+        with pytest.raises(cheb.ChebError) as e:
+            cheb.cheb_cache_begin_push(h)       # a fused push needs contiguous slots
+        assert e.value.code == B.CHEB_E_INVAL
+        with pytest.raises(cheb.ChebError) as e:
+            cheb.cheb_extrapolate(h, [1.0 / 6] * 6, FAKE_ARENA + (1 << 36), 0)
+        assert e.value.code == B.CHEB_E_NOTREADY
+    finally:
+        cheb.cheb_cache_destroy(h)
+    h = cheb.cheb_cache_create(6, B.CHEB_F32, seg, FAKE_ARENA,
+                               cheb.cheb_cache_arena_bytes_ex(6, B.CHEB_F32, seg,
+                                                              B.CHEB_LAYOUT_SLOTS))
+    try:
+        assert cheb.cheb_cache_geometry(h) == (B.CHEB_LAYOUT_SLOTS, 8192, 8192)
+    finally:
+        cheb.cheb_cache_destroy(h)
