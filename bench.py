@@ -498,11 +498,17 @@ def stream_ceilings(torch, slots_cache, il_cache, out, reps=10, warmup=2):
     buffers, one entry-sized stream each, timed per launch with HIP events on
     the current stream: six entries read, a copy, a write, and six entries
     read with one stream written from the slot layout and from the
-    interleaved layout.  GB/s counts the bytes each kernel moves."""
+    interleaved layout; and the interleaved 6:1 stream with its stores
+    folded into a 64 MiB window (held by the last-level cache: the stores
+    leave each XCD but not the chip) or a 1 MiB window (held by the XCDs'
+    L2: the stores stay in the XCD).  GB/s counts the bytes each kernel
+    would move with every store reaching HBM, so the windows read as the
+    rate the reads allow when the stores cost less."""
     import ctypes
     lib = ctypes.CDLL(CEILING_LIB)
     lib.ceiling_stream.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_void_p), ctypes.c_int,
-                                   ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
+                                   ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
+                                   ctypes.c_void_p]
     lib.ceiling_stream.restype = ctypes.c_int
     import paper_2608_23429_amd as cheb
     stream = torch.cuda.current_stream()
@@ -513,19 +519,23 @@ def stream_ceilings(torch, slots_cache, il_cache, out, reps=10, warmup=2):
     slots = [slots_cache.arena.data_ptr() + k * slots_cache.slot_stride_bytes for k in range(n)]
     # the interleaved region starts at its lowest lane
     region = min(cheb.cheb_cache_entry(il_cache.handle, a) for a in range(n))
+    # (name, kind, sources, bytes counted, store window in vectors)
     cases = [
-        ("read_only_6", 0, slots, n * S),
-        ("copy", 1, slots[:1], 2 * S),
-        ("write_only", 3, [], S),
-        ("mix_6_1_slots", 1, slots, (n + 1) * S),
-        ("mix_6_1_interleaved", 2, [region], (n + 1) * S),
+        ("read_only_6", 0, slots, n * S, 0),
+        ("read_only_6_interleaved", 4, [region], n * S, 0),
+        ("copy", 1, slots[:1], 2 * S, 0),
+        ("write_only", 3, [], S, 0),
+        ("mix_6_1_slots", 1, slots, (n + 1) * S, 0),
+        ("mix_6_1_interleaved", 2, [region], (n + 1) * S, 0),
+        ("mix_6_1_interleaved_stores_in_64MiB", 5, [region], (n + 1) * S, (64 << 20) // 16),
+        ("mix_6_1_interleaved_stores_in_1MiB", 5, [region], (n + 1) * S, (1 << 20) // 16),
     ]
     res = {}
-    for name, kind, src, nbytes in cases:
+    for name, kind, src, nbytes, window in cases:
         arr = (ctypes.c_void_p * max(1, len(src)))(*src) if src else None
-        n_src = n if kind == 2 else max(1, len(src))
+        n_src = n if kind in (2, 4, 5) else max(1, len(src))
         def launch():
-            rc = lib.ceiling_stream(kind, arr, n_src, out.data_ptr(), n_vec, handle)
+            rc = lib.ceiling_stream(kind, arr, n_src, out.data_ptr(), n_vec, window, handle)
             if rc != 0:
                 raise RuntimeError(f"ceiling_stream({name}) returned {rc}")
         for _ in range(warmup):

@@ -14,6 +14,11 @@
 //           lane k of chunk c at (c * n_src + k) chunks from src[0]), write
 //           one contiguous stream
 //   kind 3  write one stream
+//   kind 4  read as kind 2, no store (interleaved read-only)
+//   kind 5  read as kind 2, store with plain (cached) stores into a window of
+//           window_vecs vectors at dst, wrapping: sized to stay in the
+//           XCDs' L2 or in the last-level cache, it shows what the stores
+//           cost when they leave the L2 but not the chip, or not the XCD
 // Built by __graft_entry__.build() into bench_ceiling.so beside this file;
 // only bench.py loads it.
 #include <hip/hip_runtime.h>
@@ -34,13 +39,13 @@ struct Srcs {
 
 template <int NS, int KIND>
 __global__ __launch_bounds__(kBlock) void stream_kernel(Srcs s, u32x4 *__restrict__ dst,
-                                                        uint32_t n_vec) {
+                                                        uint32_t n_vec, uint32_t window_mask) {
   const uint32_t i = blockIdx.x * uint32_t(kBlock) + threadIdx.x;
   if (i >= n_vec) return;
   u32x4 x = {i, 0u, 0u, 0u};
   if constexpr (KIND != 3) {
     u32x4 v[NS];
-    if constexpr (KIND == 2) {
+    if constexpr (KIND == 2 || KIND == 4 || KIND == 5) {
       const uint64_t base = uint64_t(i >> kChunkShift) * uint64_t(NS) * kChunkVecs +
                             (i & (kChunkVecs - 1));
 #pragma unroll
@@ -54,21 +59,24 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(Srcs s, u32x4 *__restric
 #pragma unroll
     for (int k = 1; k < NS; ++k) x ^= v[k];
   }
-  if constexpr (KIND == 0) {
+  if constexpr (KIND == 0 || KIND == 4) {
     // Taken only if four words match a fixed pattern; dst[i] is in bounds.
     if (x[0] == 0x9e3779b9u && x[1] == 0x7f4a7c15u && x[2] == 0xf39cc060u && x[3] == 0x5ced7e1bu)
       dst[i] = x;
+  } else if constexpr (KIND == 5) {
+    dst[i & window_mask] = x;
   } else {
     __builtin_nontemporal_store(x, dst + i);
   }
 }
 
 template <int KIND>
-hipError_t launch_kind(int n_src, const Srcs &s, u32x4 *dst, uint32_t n_vec, hipStream_t st) {
+hipError_t launch_kind(int n_src, const Srcs &s, u32x4 *dst, uint32_t n_vec, uint32_t mask,
+                       hipStream_t st) {
   const dim3 grid((n_vec + kBlock - 1) / kBlock);
   switch (n_src) {
 #define CEIL_CASE(N) \
-  case N: hipLaunchKernelGGL((stream_kernel<N, KIND>), grid, dim3(kBlock), 0, st, s, dst, n_vec); break;
+  case N: hipLaunchKernelGGL((stream_kernel<N, KIND>), grid, dim3(kBlock), 0, st, s, dst, n_vec, mask); break;
     CEIL_CASE(1) CEIL_CASE(2) CEIL_CASE(3) CEIL_CASE(4) CEIL_CASE(5) CEIL_CASE(6) CEIL_CASE(7)
     CEIL_CASE(8)
 #undef CEIL_CASE
@@ -80,35 +88,43 @@ hipError_t launch_kind(int n_src, const Srcs &s, u32x4 *dst, uint32_t n_vec, hip
 }  // namespace
 
 // Launches one ceiling kernel over n_vec 16-byte vectors on `stream`.
-//   kind   0..3 as above; n_src 1..8 (ignored for kind 3).
+//   kind   0..5 as above; n_src 1..8 (ignored for kind 3).
 //   src    [n_src] device pointers, 16-byte aligned, n_vec vectors each
-//          (kind 2: src[0] is the interleaved region, n_src * n_vec vectors
-//          rounded up to whole chunks per lane).
-//   dst    device pointer to n_vec vectors (kind 0: written only in the
-//          never-taken case).
+//          (kinds 2, 4, 5: src[0] is the interleaved region, n_src * n_vec
+//          vectors rounded up to whole chunks per lane).
+//   dst    device pointer to n_vec vectors (kinds 0 and 4: written only in
+//          the never-taken case; kind 5: window_vecs vectors).
+//   window_vecs  kind 5 only: a power of two, 1 .. n_vec.
 // Returns 0, or -1 for arguments out of range, or the HIP error code of the
 // launch.
 extern "C" __attribute__((visibility("default"))) int ceiling_stream(int kind, const void *const *src,
                                                                      int n_src, void *dst,
-                                                                     int64_t n_vec, void *stream) {
-  if (kind < 0 || kind > 3 || n_vec < 0 || n_vec >= (int64_t(1) << 31) || !dst) return -1;
+                                                                     int64_t n_vec,
+                                                                     int64_t window_vecs,
+                                                                     void *stream) {
+  if (kind < 0 || kind > 5 || n_vec < 0 || n_vec >= (int64_t(1) << 31) || !dst) return -1;
+  if (kind == 5 && (window_vecs < 1 || window_vecs > n_vec || (window_vecs & (window_vecs - 1))))
+    return -1;
   if (kind != 3 && (n_src < 1 || n_src > 8 || !src)) return -1;
   if (n_vec == 0) return 0;
   Srcs s = {};
   if (kind != 3)
-    for (int k = 0; k < (kind == 2 ? 1 : n_src); ++k) {
+    for (int k = 0; k < (kind == 2 || kind == 4 || kind == 5 ? 1 : n_src); ++k) {
       if (!src[k]) return -1;
       s.p[k] = static_cast<const u32x4 *>(src[k]);
     }
   u32x4 *d = static_cast<u32x4 *>(dst);
   const uint32_t n = uint32_t(n_vec);
+  const uint32_t mask = kind == 5 ? uint32_t(window_vecs - 1) : 0u;
   hipStream_t st = static_cast<hipStream_t>(stream);
   hipError_t e;
   switch (kind) {
-    case 0: e = launch_kind<0>(n_src, s, d, n, st); break;
-    case 1: e = launch_kind<1>(n_src, s, d, n, st); break;
-    case 2: e = launch_kind<2>(n_src, s, d, n, st); break;
-    default: e = launch_kind<3>(1, s, d, n, st); break;
+    case 0: e = launch_kind<0>(n_src, s, d, n, mask, st); break;
+    case 1: e = launch_kind<1>(n_src, s, d, n, mask, st); break;
+    case 2: e = launch_kind<2>(n_src, s, d, n, mask, st); break;
+    case 4: e = launch_kind<4>(n_src, s, d, n, mask, st); break;
+    case 5: e = launch_kind<5>(n_src, s, d, n, mask, st); break;
+    default: e = launch_kind<3>(1, s, d, n, mask, st); break;
   }
   return e == hipSuccess ? 0 : int(e);
 }
