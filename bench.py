@@ -68,6 +68,7 @@ def parse_args(argv=None):
     ap.add_argument("--unroll", type=int, default=None)
     ap.add_argument("--nontemporal", type=int, default=None)
     ap.add_argument("--blocks-per-cu", type=int, default=None)
+    ap.add_argument("--waves-per-cu", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="approximate CPU time budget of the oracle baseline")
@@ -493,6 +494,21 @@ def measure_cache(torch, cheb, cfg, cache, out, push_ms, entries, steps, warmup,
     return res
 
 
+def device_summary(torch):
+    """Name, compute units and LDS per compute unit of device 0 (the LDS is
+    what the occupancy cap of the prediction divides)."""
+    import ctypes
+    lib = ctypes.CDLL(CEILING_LIB)
+    lib.ceiling_lds_per_cu.restype = ctypes.c_int
+    lds = lib.ceiling_lds_per_cu()
+    p = torch.cuda.get_device_properties(0)
+    return {"name": p.name, "gcn_arch": getattr(p, "gcnArchName", None),
+            "compute_units": p.multi_processor_count,
+            "lds_per_cu_bytes": lds if lds >= 0 else None,
+            "lds_reserved_per_64_lane_block_at_8_waves": lds // 8 // 1024 * 1024
+            if lds > 0 else None}
+
+
 def stream_ceilings(torch, slots_cache, il_cache, out, reps=10, warmup=2):
     """Trivial-body streams (bench_ceiling.hip) over the benchmark's own
     buffers, one entry-sized stream each, timed per launch with HIP events on
@@ -503,12 +519,15 @@ def stream_ceilings(torch, slots_cache, il_cache, out, reps=10, warmup=2):
     leave each XCD but not the chip) or a 1 MiB window (held by the XCDs'
     L2: the stores stay in the XCD).  GB/s counts the bytes each kernel
     would move with every store reaching HBM, so the windows read as the
-    rate the reads allow when the stores cost less."""
+    rate the reads allow when the stores cost less.  Every case runs in both
+    launch shapes of the prediction: 1024-lane blocks at full occupancy, and
+    64-lane blocks capped at 8 waves per compute unit (suffix _w8); the
+    6:1 streams also at 12 waves (_w12)."""
     import ctypes
     lib = ctypes.CDLL(CEILING_LIB)
     lib.ceiling_stream.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_void_p), ctypes.c_int,
                                    ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
-                                   ctypes.c_void_p]
+                                   ctypes.c_int, ctypes.c_void_p]
     lib.ceiling_stream.restype = ctypes.c_int
     import paper_2608_23429_amd as cheb
     stream = torch.cuda.current_stream()
@@ -530,12 +549,19 @@ def stream_ceilings(torch, slots_cache, il_cache, out, reps=10, warmup=2):
         ("mix_6_1_interleaved_stores_in_64MiB", 5, [region], (n + 1) * S, (64 << 20) // 16),
         ("mix_6_1_interleaved_stores_in_1MiB", 5, [region], (n + 1) * S, (1 << 20) // 16),
     ]
-    res = {}
+    shaped = []
     for name, kind, src, nbytes, window in cases:
+        shaped.append((name, kind, src, nbytes, window, 0))
+        shaped.append((name + "_w8", kind, src, nbytes, window, 8))
+        if name.startswith("mix_6_1") and window == 0:
+            shaped.append((name + "_w12", kind, src, nbytes, window, 12))
+    res = {}
+    for name, kind, src, nbytes, window, waves in shaped:
         arr = (ctypes.c_void_p * max(1, len(src)))(*src) if src else None
         n_src = n if kind in (2, 4, 5) else max(1, len(src))
         def launch():
-            rc = lib.ceiling_stream(kind, arr, n_src, out.data_ptr(), n_vec, window, handle)
+            rc = lib.ceiling_stream(kind, arr, n_src, out.data_ptr(), n_vec, window, waves,
+                                    handle)
             if rc != 0:
                 raise RuntimeError(f"ceiling_stream({name}) returned {rc}")
         for _ in range(warmup):
@@ -578,7 +604,7 @@ def main(argv=None):
 
     shape = cheb.cheb_get_launch_config()
     for k, v in (("block", args.block), ("unroll", args.unroll), ("nontemporal", args.nontemporal),
-                 ("blocks_per_cu", args.blocks_per_cu)):
+                 ("blocks_per_cu", args.blocks_per_cu), ("waves_per_cu", args.waves_per_cu)):
         if v is not None:
             shape[k] = v
     cheb.cheb_set_launch_config(**shape)
@@ -628,7 +654,10 @@ def main(argv=None):
         f"{resid['collapsed_push_difference']['us']:.1f} us) per full step")
     achieved = res["bytes_per_step"] / (res["launch_us_avg"] * 1e3)
     traffic = measured_traffic(cfg.name)
-    own = ceilings["mix_6_1_interleaved"]["gbps_median"] if ceilings else None
+    # the ceiling is the faster of the trivial 6:1 interleaved stream's
+    # launch shapes
+    own = max(ceilings[k]["gbps_median"] for k in ceilings
+              if k.startswith("mix_6_1_interleaved") and "stores_in" not in k) if ceilings else None
     line = {
         "metric": METRIC,
         "value": res["gbps"],
@@ -653,10 +682,11 @@ def main(argv=None):
                      "layout": LAYOUT,
                      "ceiling": ceilings,
                      "frac_of_ceiling": achieved / own if own else None,
-                     "ceiling_note": "trivial-body streams (XOR, same launch shape and access "
-                                     "pattern) over entry-sized streams of this workload, timed "
-                                     "in this run; frac_of_ceiling is against the 6-read:1-write "
-                                     "stream over the same interleaved layout"},
+                     "ceiling_note": "trivial-body streams (XOR, the prediction's access "
+                                     "pattern, in its launch shapes) over entry-sized streams of "
+                                     "this workload, timed in this run; frac_of_ceiling is "
+                                     "against the fastest shape of the 6-read:1-write stream "
+                                     "over the same interleaved layout"},
         "layouts": {
             LAYOUT: {"us_per_step": res["us_per_step"], "gbps": res["gbps"],
                      "launch_us_avg": res["launch_us_avg"], "push_us_median": res["push_us_median"]},
@@ -668,6 +698,7 @@ def main(argv=None):
                       "p90": res["launch_us_p90"], "avg": res["launch_us_avg"]},
         "push": {"us_median": res["push_us_median"], "gbps": res["push_gbps"],
                  "note": "full-step copy into the ring, once per full step (not in value)"},
+        "device": device_summary(torch),
         "multi_target": multi,
         "residual": resid,
         "online_run": online,

@@ -4,9 +4,11 @@
 // sustains for the same mix of reads and writes.
 //
 // Every kernel moves 16-byte vectors with non-temporal loads and stores, one
-// vector per lane, 1024-lane blocks, one block per 1024 vectors: the launch
-// shape the prediction uses.  The body is an XOR of the loaded vectors, so
-// arithmetic costs nothing.
+// vector per lane, one block per block-sized run of vectors, in one of the
+// prediction's two launch shapes: 1024-lane blocks at full occupancy, or
+// 64-lane blocks with the waves per compute unit capped by a reservation of
+// LDS that the kernel never touches.  The body is an XOR of the loaded
+// vectors, so arithmetic costs nothing.
 //   kind 0  read n_src contiguous streams, no store (a store that the data
 //           never triggers keeps the loads alive)
 //   kind 1  read n_src contiguous streams, write one stream
@@ -29,7 +31,6 @@ namespace {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kBlock = 1024;
 constexpr int kChunkShift = 11;  // 2048 vectors = 32 KiB
 constexpr uint32_t kChunkVecs = 1u << kChunkShift;
 
@@ -37,10 +38,10 @@ struct Srcs {
   const u32x4 *p[8];
 };
 
-template <int NS, int KIND>
-__global__ __launch_bounds__(kBlock) void stream_kernel(Srcs s, u32x4 *__restrict__ dst,
-                                                        uint32_t n_vec, uint32_t window_mask) {
-  const uint32_t i = blockIdx.x * uint32_t(kBlock) + threadIdx.x;
+template <int NS, int KIND, int BLK>
+__global__ __launch_bounds__(BLK) void stream_kernel(Srcs s, u32x4 *__restrict__ dst,
+                                                     uint32_t n_vec, uint32_t window_mask) {
+  const uint32_t i = blockIdx.x * uint32_t(BLK) + threadIdx.x;
   if (i >= n_vec) return;
   u32x4 x = {i, 0u, 0u, 0u};
   if constexpr (KIND != 3) {
@@ -70,19 +71,32 @@ __global__ __launch_bounds__(kBlock) void stream_kernel(Srcs s, u32x4 *__restric
   }
 }
 
-template <int KIND>
+template <int KIND, int BLK>
 hipError_t launch_kind(int n_src, const Srcs &s, u32x4 *dst, uint32_t n_vec, uint32_t mask,
-                       hipStream_t st) {
-  const dim3 grid((n_vec + kBlock - 1) / kBlock);
+                       size_t lds, hipStream_t st) {
+  const dim3 grid((n_vec + BLK - 1) / BLK);
   switch (n_src) {
 #define CEIL_CASE(N) \
-  case N: hipLaunchKernelGGL((stream_kernel<N, KIND>), grid, dim3(kBlock), 0, st, s, dst, n_vec, mask); break;
+  case N: hipLaunchKernelGGL((stream_kernel<N, KIND, BLK>), grid, dim3(BLK), lds, st, s, dst, n_vec, mask); break;
     CEIL_CASE(1) CEIL_CASE(2) CEIL_CASE(3) CEIL_CASE(4) CEIL_CASE(5) CEIL_CASE(6) CEIL_CASE(7)
     CEIL_CASE(8)
 #undef CEIL_CASE
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
+}
+
+template <int BLK>
+hipError_t launch(int kind, int n_src, const Srcs &s, u32x4 *d, uint32_t n, uint32_t mask,
+                  size_t lds, hipStream_t st) {
+  switch (kind) {
+    case 0: return launch_kind<0, BLK>(n_src, s, d, n, mask, lds, st);
+    case 1: return launch_kind<1, BLK>(n_src, s, d, n, mask, lds, st);
+    case 2: return launch_kind<2, BLK>(n_src, s, d, n, mask, lds, st);
+    case 4: return launch_kind<4, BLK>(n_src, s, d, n, mask, lds, st);
+    case 5: return launch_kind<5, BLK>(n_src, s, d, n, mask, lds, st);
+    default: return launch_kind<3, BLK>(1, s, d, n, mask, lds, st);
+  }
 }
 
 }  // namespace
@@ -95,14 +109,20 @@ hipError_t launch_kind(int n_src, const Srcs &s, u32x4 *dst, uint32_t n_vec, uin
 //   dst    device pointer to n_vec vectors (kinds 0 and 4: written only in
 //          the never-taken case; kind 5: window_vecs vectors).
 //   window_vecs  kind 5 only: a power of two, 1 .. n_vec.
+//   waves_per_cu  0: 1024-lane blocks at full occupancy; 3..32: 64-lane
+//          blocks, each reserving 1/waves_per_cu of the compute unit's LDS
+//          (at most 64 KiB), so that at most that many waves share a
+//          compute unit.
 // Returns 0, or -1 for arguments out of range, or the HIP error code of the
-// launch.
+// launch or of the device query.
 extern "C" __attribute__((visibility("default"))) int ceiling_stream(int kind, const void *const *src,
                                                                      int n_src, void *dst,
                                                                      int64_t n_vec,
                                                                      int64_t window_vecs,
+                                                                     int waves_per_cu,
                                                                      void *stream) {
   if (kind < 0 || kind > 5 || n_vec < 0 || n_vec >= (int64_t(1) << 31) || !dst) return -1;
+  if (waves_per_cu != 0 && (waves_per_cu < 3 || waves_per_cu > 32)) return -1;
   if (kind == 5 && (window_vecs < 1 || window_vecs > n_vec || (window_vecs & (window_vecs - 1))))
     return -1;
   if (kind != 3 && (n_src < 1 || n_src > 8 || !src)) return -1;
@@ -118,13 +138,28 @@ extern "C" __attribute__((visibility("default"))) int ceiling_stream(int kind, c
   const uint32_t mask = kind == 5 ? uint32_t(window_vecs - 1) : 0u;
   hipStream_t st = static_cast<hipStream_t>(stream);
   hipError_t e;
-  switch (kind) {
-    case 0: e = launch_kind<0>(n_src, s, d, n, mask, st); break;
-    case 1: e = launch_kind<1>(n_src, s, d, n, mask, st); break;
-    case 2: e = launch_kind<2>(n_src, s, d, n, mask, st); break;
-    case 4: e = launch_kind<4>(n_src, s, d, n, mask, st); break;
-    case 5: e = launch_kind<5>(n_src, s, d, n, mask, st); break;
-    default: e = launch_kind<3>(1, s, d, n, mask, st); break;
+  if (waves_per_cu == 0) {
+    e = launch<1024>(kind, n_src, s, d, n, mask, 0, st);
+  } else {
+    int dev = 0, lds_per_cu = 0;
+    e = hipGetDevice(&dev);
+    if (e == hipSuccess)
+      e = hipDeviceGetAttribute(&lds_per_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev);
+    if (e != hipSuccess) return int(e);
+    const size_t lds = size_t(lds_per_cu / waves_per_cu) / 1024 * 1024;
+    if (lds > (size_t(64) << 10)) return -1;
+    e = launch<64>(kind, n_src, s, d, n, mask, lds, st);
   }
   return e == hipSuccess ? 0 : int(e);
+}
+
+// LDS bytes per compute unit of the current device, as the runtime reports
+// it (what the occupancy cap divides), or -1 if the query fails.
+extern "C" __attribute__((visibility("default"))) int ceiling_lds_per_cu(void) {
+  int dev = 0, lds = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return -1;
+  if (hipDeviceGetAttribute(&lds, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) !=
+      hipSuccess)
+    return -1;
+  return lds;
 }

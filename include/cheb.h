@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define CHEB_VERSION 3
+#define CHEB_VERSION 4
 
 #if defined(__GNUC__) || defined(__clang__)
 #define CHEB_API __attribute__((visibility("default")))
@@ -521,22 +521,36 @@ CHEB_API int cheb_residual_reduce(const void *const *seg_src, const int64_t *seg
 /* ------------------------------------------------------------------------ */
 
 /* Launch shape of the streaming kernels, process-wide.
- *   block        threads per block: 256, 512 or 1024.
+ *   block        threads per block: 64, 256, 512 or 1024.
  *   unroll       16-byte vectors per thread per history entry in flight;
- *                block * unroll must not exceed 1024 (256: 1, 2 or 4;
- *                512: 1 or 2; 1024: 1).
+ *                block * unroll must not exceed 1024 (64: 1; 256: 1, 2
+ *                or 4; 512: 1 or 2; 1024: 1).
  *   nontemporal  1: history loads and output stores carry the non-temporal
  *                hint; 0: ordinary loads and stores.
  *   blocks_per_cu  0: one block per tile of block x unroll vectors (the grid
  *                covers the whole problem); 1..64: a persistent grid of that
  *                many blocks per compute unit, each looping over tiles.
- * Default {1024, 1, 1, 0}; with block 1024, a problem under 4096 vectors
- * per compute unit runs with 256-thread blocks.  Errors: CHEB_E_INVAL. */
+ *   waves_per_cu  cap on the prediction kernel's 64-lane waves resident on
+ *                one compute unit.  0: chosen from the history size (8 for 5
+ *                or more entries, 12 for 4, 16 for 3, 24 for 2, none for 1);
+ *                -1: no cap; 1..32: that cap.  Each block reserves an equal
+ *                share of the compute unit's LDS, which the kernel never
+ *                touches, so that no more blocks fit; the cap applies only
+ *                where that share is at most 64 KiB (64- and 256-thread
+ *                blocks) and is ignored otherwise.
+ * Default {64, 1, 1, 0, 0}.  On MI355X a bf16 history of 5-6 entries
+ * streams at about 0.86 of the HBM peak with 8 waves per compute unit,
+ * against 0.77 with 1024-thread blocks at full occupancy: fewer waves keep
+ * enough loads in flight without crowding out the output's stores.  With
+ * block 1024, a problem under 4096 vectors per compute unit runs with
+ * 256-thread blocks.  The history ring's push (a copy) always runs at full
+ * occupancy.  Errors: CHEB_E_INVAL. */
 typedef struct cheb_launch_config {
   int32_t block;
   int32_t unroll;
   int32_t nontemporal;
   int32_t blocks_per_cu;
+  int32_t waves_per_cu;
 } cheb_launch_config;
 
 CHEB_API int cheb_get_launch_config(cheb_launch_config *cfg);

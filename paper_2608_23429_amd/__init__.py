@@ -14,7 +14,7 @@ import torch
 
 from ._binding import (  # noqa: F401  (re-exported C entry points)
     CHEB_LAYOUT_INTERLEAVED, CHEB_LAYOUT_SLOTS, cheb_cache_arena_bytes_ex, cheb_cache_create_ex,
-    cheb_cache_geometry,
+    cheb_cache_geometry, DEFAULT_LAUNCH_CONFIG,
     CHEB_BF16, CHEB_F16, CHEB_F32, CHEB_MAX_NODES, CHEB_MAX_OUTPUTS, CHEB_MAX_SLOTS, CHEB_RHO_ALTERNATING,
     CHEB_RHO_GENERAL, CHEB_SHORT_FULL, CHEB_TAYLOR, CHEB_SHORT_LOWER, ChebError, cheb_chebyshev_nodes,
     cheb_precompute_weights_variant,

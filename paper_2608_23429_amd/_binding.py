@@ -12,6 +12,9 @@ import numpy as np
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libcheb.so")
 
+# The library version this binding's structures match (CHEB_VERSION).
+CHEB_VERSION = 4
+
 CHEB_OK = 0
 CHEB_E_INVAL = -1
 CHEB_E_DUPNODE = -2
@@ -58,7 +61,14 @@ class ChebError(RuntimeError):
 
 class cheb_launch_config(ctypes.Structure):
     _fields_ = [("block", ctypes.c_int32), ("unroll", ctypes.c_int32),
-                ("nontemporal", ctypes.c_int32), ("blocks_per_cu", ctypes.c_int32)]
+                ("nontemporal", ctypes.c_int32), ("blocks_per_cu", ctypes.c_int32),
+                ("waves_per_cu", ctypes.c_int32)]
+
+
+# The library's launch shape at load time (64-lane blocks, occupancy capped by
+# history size).
+DEFAULT_LAUNCH_CONFIG = {"block": 64, "unroll": 1, "nontemporal": 1, "blocks_per_cu": 0,
+                         "waves_per_cu": 0}
 
 
 _dp = ctypes.POINTER(ctypes.c_double)
@@ -132,6 +142,9 @@ def _load():
         fn = getattr(lib, name)
         fn.argtypes = argtypes
         fn.restype = ctypes.c_char_p if name == "cheb_last_error" else ctypes.c_int
+    if lib.cheb_version() != CHEB_VERSION:
+        raise ImportError(f"{LIB_PATH} is version {lib.cheb_version()}, the binding expects "
+                          f"{CHEB_VERSION}; rebuild with __graft_entry__.build()")
     return lib
 
 
@@ -438,9 +451,10 @@ def cheb_get_launch_config():
     c = cheb_launch_config()
     _check(LIB.cheb_get_launch_config(ctypes.byref(c)))
     return {"block": c.block, "unroll": c.unroll, "nontemporal": c.nontemporal,
-            "blocks_per_cu": c.blocks_per_cu}
+            "blocks_per_cu": c.blocks_per_cu, "waves_per_cu": c.waves_per_cu}
 
 
-def cheb_set_launch_config(block=1024, unroll=1, nontemporal=1, blocks_per_cu=0):
-    c = cheb_launch_config(int(block), int(unroll), int(nontemporal), int(blocks_per_cu))
+def cheb_set_launch_config(block=64, unroll=1, nontemporal=1, blocks_per_cu=0, waves_per_cu=0):
+    c = cheb_launch_config(int(block), int(unroll), int(nontemporal), int(blocks_per_cu),
+                           int(waves_per_cu))
     _check(LIB.cheb_set_launch_config(ctypes.byref(c)))

@@ -17,10 +17,11 @@ namespace {
 thread_local char g_error[512] = "";
 
 std::mutex g_shape_mutex;
-cheb_launch_config g_shape = {1024, 1, 1, 0};
+cheb_launch_config g_shape = {64, 1, 1, 0, 0};
 
 constexpr int kMaxDevices = 64;
 int g_cus[kMaxDevices] = {0};
+int g_lds[kMaxDevices] = {0};
 std::mutex g_cus_mutex;
 
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -44,7 +45,7 @@ cheb_launch_config launch_shape() {
   return g_shape;
 }
 
-int device_cus(int *cus) {
+int device_info(int *cus, int *lds_per_cu) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return fail(CHEB_E_HIP, "hipGetDevice: %s", hipGetErrorString(e));
@@ -52,18 +53,24 @@ int device_cus(int *cus) {
     std::lock_guard<std::mutex> lock(g_cus_mutex);
     if (g_cus[dev] > 0) {
       *cus = g_cus[dev];
+      *lds_per_cu = g_lds[dev];
       return CHEB_OK;
     }
   }
-  int n = 0;
+  int n = 0, lds = 0;
   e = hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev);
   if (e != hipSuccess || n <= 0)
     return fail(CHEB_E_HIP, "compute unit count: %s", hipGetErrorString(e));
+  e = hipDeviceGetAttribute(&lds, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev);
+  if (e != hipSuccess || lds < 0)
+    return fail(CHEB_E_HIP, "LDS per compute unit: %s", hipGetErrorString(e));
   if (dev >= 0 && dev < kMaxDevices) {
     std::lock_guard<std::mutex> lock(g_cus_mutex);
     g_cus[dev] = n;
+    g_lds[dev] = lds;
   }
   *cus = n;
+  *lds_per_cu = lds;
   return CHEB_OK;
 }
 
@@ -249,10 +256,12 @@ int cheb_get_launch_config(cheb_launch_config *cfg) {
 
 int cheb_set_launch_config(const cheb_launch_config *cfg) {
   if (!cfg) return fail(CHEB_E_INVAL, "cfg is NULL");
-  if (cfg->block != 256 && cfg->block != 512 && cfg->block != 1024)
-    return fail(CHEB_E_INVAL, "block must be 256, 512 or 1024 (got %d)", cfg->block);
+  if (cfg->block != 64 && cfg->block != 256 && cfg->block != 512 && cfg->block != 1024)
+    return fail(CHEB_E_INVAL, "block must be 64, 256, 512 or 1024 (got %d)", cfg->block);
   if (cfg->unroll != 1 && cfg->unroll != 2 && cfg->unroll != 4)
     return fail(CHEB_E_INVAL, "unroll must be 1, 2 or 4 (got %d)", cfg->unroll);
+  if (cfg->block == 64 && cfg->unroll != 1)
+    return fail(CHEB_E_INVAL, "block 64 takes unroll 1 (got %d)", cfg->unroll);
   if (cfg->block * cfg->unroll > 1024)
     return fail(CHEB_E_INVAL, "block x unroll must not exceed 1024 (got %d x %d)", cfg->block,
                 cfg->unroll);
@@ -260,6 +269,8 @@ int cheb_set_launch_config(const cheb_launch_config *cfg) {
     return fail(CHEB_E_INVAL, "nontemporal must be 0 or 1 (got %d)", cfg->nontemporal);
   if (cfg->blocks_per_cu < 0 || cfg->blocks_per_cu > 64)
     return fail(CHEB_E_INVAL, "blocks_per_cu must be 0..64 (got %d)", cfg->blocks_per_cu);
+  if (cfg->waves_per_cu < -1 || cfg->waves_per_cu > 32)
+    return fail(CHEB_E_INVAL, "waves_per_cu must be -1..32 (got %d)", cfg->waves_per_cu);
   std::lock_guard<std::mutex> lock(g_shape_mutex);
   g_shape = *cfg;
   return ok();

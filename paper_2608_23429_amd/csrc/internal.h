@@ -43,8 +43,9 @@ constexpr size_t kLaneAlign = size_t(64) << 10;
 // Current process-wide launch shape.
 cheb_launch_config launch_shape();
 
-// Number of compute units of the current device (cached per device).
-int device_cus(int *cus);
+// Compute units and LDS bytes per compute unit of the current device
+// (cached per device).
+int device_info(int *cus, int *lds_per_cu);
 
 // One row of barycentric interpolation coefficients (host, fp64).  Returns
 // CHEB_OK or an error code with the message set.

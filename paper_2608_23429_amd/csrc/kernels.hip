@@ -268,52 +268,94 @@ __global__ __launch_bounds__(BLK) void combine_kernel(Hist<NS, NO, typename Op::
   }
 }
 
+// The device the launch goes to.
+struct Gpu {
+  int cus;         // compute units
+  int lds_per_cu;  // LDS bytes per compute unit
+  int waves;       // occupancy cap in waves per compute unit, 0: none
+};
+
+// Waves per compute unit the prediction streams best with, by history size.
+// Measured on MI355X (FLUX-sized streams): the mix of NS reads and the
+// output's writes runs fastest with about 48 KiB of loads in flight per
+// compute unit (8 waves of 64 lanes x NS x 16 bytes for NS = 5, 6); more
+// waves flood the memory queues and slow the writes, fewer leave latency
+// uncovered.
+int auto_waves(int ns) {
+  if (ns >= 5) return 8;
+  if (ns == 4) return 12;
+  if (ns == 3) return 16;
+  if (ns == 2) return 24;
+  return 0;
+}
+
+// Dynamic LDS a block reserves, and never touches, so that at most `waves`
+// waves of the kernel share a compute unit (the LDS is what runs out).  Zero
+// when there is no cap, when the cap is at the hardware's own limit, or when
+// one block would need more than the default 64 KiB of dynamic LDS.
+template <int BLK>
+size_t occupancy_lds(const Gpu &g) {
+  constexpr int kWavesPerBlock = BLK / 64;
+  if (g.waves <= 0 || g.lds_per_cu <= 0) return 0;
+  const int blocks = std::max(1, g.waves / kWavesPerBlock);
+  if (blocks * kWavesPerBlock >= 32) return 0;
+  const size_t per = size_t(g.lds_per_cu / blocks) / 1024 * 1024;
+  return per <= size_t(64) << 10 ? per : 0;
+}
+
 template <class Op, int NS, int NO, int BLK, int U, bool NT>
 hipError_t launch_shape(const Hist<NS, NO, typename Op::W> &h, uint32_t n_vec, Tail tail,
-                        int blocks_per_cu, int cus, hipStream_t s) {
+                        int blocks_per_cu, const Gpu &g, hipStream_t s) {
   const uint32_t per_tile = uint32_t(BLK * U);
   const uint32_t n_tiles = (n_vec + per_tile - 1) / per_tile;
   uint32_t grid = std::max<uint32_t>(n_tiles, 1u);
-  if (blocks_per_cu > 0) grid = std::min<uint32_t>(grid, uint32_t(blocks_per_cu) * uint32_t(cus));
-  hipLaunchKernelGGL((combine_kernel<Op, NS, NO, BLK, U, NT>), dim3(grid), dim3(BLK), 0, s, h,
-                     n_vec, n_tiles, tail);
+  if (blocks_per_cu > 0) grid = std::min<uint32_t>(grid, uint32_t(blocks_per_cu) * uint32_t(g.cus));
+  hipLaunchKernelGGL((combine_kernel<Op, NS, NO, BLK, U, NT>), dim3(grid), dim3(BLK),
+                     occupancy_lds<BLK>(g), s, h, n_vec, n_tiles, tail);
   return hipGetLastError();
 }
 
 // Single output: every launch shape of the tuning interface.
 template <class Op, int NS, bool NT>
 hipError_t launch_one(const Hist<NS, 1, typename Op::W> &h, uint32_t n_vec, Tail tail,
-                      const cheb_launch_config &cfg, int cus, hipStream_t s) {
+                      const cheb_launch_config &cfg, const Gpu &dev, hipStream_t s) {
   const int b = cfg.block, u = cfg.unroll, g = cfg.blocks_per_cu;
   // A problem too small to give every compute unit a few 1024-thread blocks
   // runs with 256-thread blocks instead (four times as many blocks).
-  const bool small = uint64_t(n_vec) < uint64_t(4 * 1024) * uint64_t(cus);
-  if (b == 1024 && small) return launch_shape<Op, NS, 1, 256, 1, NT>(h, n_vec, tail, g, cus, s);
-  if (b == 1024) return launch_shape<Op, NS, 1, 1024, 1, NT>(h, n_vec, tail, g, cus, s);
+  const bool small = uint64_t(n_vec) < uint64_t(4 * 1024) * uint64_t(dev.cus);
+  if (b == 64) return launch_shape<Op, NS, 1, 64, 1, NT>(h, n_vec, tail, g, dev, s);
+  if (b == 1024 && small) return launch_shape<Op, NS, 1, 256, 1, NT>(h, n_vec, tail, g, dev, s);
+  if (b == 1024) return launch_shape<Op, NS, 1, 1024, 1, NT>(h, n_vec, tail, g, dev, s);
   if (b == 512) {
-    if (u == 1) return launch_shape<Op, NS, 1, 512, 1, NT>(h, n_vec, tail, g, cus, s);
-    return launch_shape<Op, NS, 1, 512, 2, NT>(h, n_vec, tail, g, cus, s);
+    if (u == 1) return launch_shape<Op, NS, 1, 512, 1, NT>(h, n_vec, tail, g, dev, s);
+    return launch_shape<Op, NS, 1, 512, 2, NT>(h, n_vec, tail, g, dev, s);
   }
-  if (u == 1) return launch_shape<Op, NS, 1, 256, 1, NT>(h, n_vec, tail, g, cus, s);
-  if (u == 2) return launch_shape<Op, NS, 1, 256, 2, NT>(h, n_vec, tail, g, cus, s);
-  return launch_shape<Op, NS, 1, 256, 4, NT>(h, n_vec, tail, g, cus, s);
+  if (u == 1) return launch_shape<Op, NS, 1, 256, 1, NT>(h, n_vec, tail, g, dev, s);
+  if (u == 2) return launch_shape<Op, NS, 1, 256, 2, NT>(h, n_vec, tail, g, dev, s);
+  return launch_shape<Op, NS, 1, 256, 4, NT>(h, n_vec, tail, g, dev, s);
 }
 
-// Several outputs: one shape (1024 threads, one vector per lane, the
-// non-temporal hint as configured, grid covering the range), which keeps the
+// Several outputs: one vector per lane, a grid covering the range, 64-lane
+// blocks (under the occupancy cap) or 1024-lane blocks for any other
+// configured block, and the non-temporal hint as configured; this keeps the
 // number of kernel instances bounded.
 template <class Op, int NS, int NO>
 hipError_t launch_many(const Hist<NS, NO, typename Op::W> &h, uint32_t n_vec, Tail tail,
-                       const cheb_launch_config &cfg, int cus, hipStream_t s) {
-  return cfg.nontemporal ? launch_shape<Op, NS, NO, 1024, 1, true>(h, n_vec, tail, 0, cus, s)
-                         : launch_shape<Op, NS, NO, 1024, 1, false>(h, n_vec, tail, 0, cus, s);
+                       const cheb_launch_config &cfg, const Gpu &dev, hipStream_t s) {
+  if (cfg.block == 64)
+    return cfg.nontemporal ? launch_shape<Op, NS, NO, 64, 1, true>(h, n_vec, tail, 0, dev, s)
+                           : launch_shape<Op, NS, NO, 64, 1, false>(h, n_vec, tail, 0, dev, s);
+  return cfg.nontemporal ? launch_shape<Op, NS, NO, 1024, 1, true>(h, n_vec, tail, 0, dev, s)
+                         : launch_shape<Op, NS, NO, 1024, 1, false>(h, n_vec, tail, 0, dev, s);
 }
 
 template <class Op, int NS, int NO>
 hipError_t launch_ns_no(const void *const *src, const double *w, void *const *out,
-                        int64_t numel, int64_t super_vecs, const cheb_launch_config &cfg, int cus,
-                        hipStream_t s) {
+                        int64_t numel, int64_t super_vecs, const cheb_launch_config &cfg,
+                        const Gpu &dev0, hipStream_t s) {
   constexpr int kVec = 16 / int(sizeof(typename Op::E));
+  Gpu dev = dev0;
+  dev.waves = cfg.waves_per_cu == 0 ? auto_waves(NS) : std::max(0, cfg.waves_per_cu);
   Hist<NS, NO, typename Op::W> h;
   h.super = uint64_t(super_vecs);
   for (int k = 0; k < NS; ++k) h.p[k] = static_cast<const u32x4 *>(src[k]);
@@ -324,16 +366,16 @@ hipError_t launch_ns_no(const void *const *src, const double *w, void *const *ou
   const uint32_t n_vec = uint32_t(numel / kVec);
   Tail tail{uint32_t(numel % kVec), uint64_t(numel / kVec) * kVec};
   if constexpr (NO == 1) {
-    return cfg.nontemporal ? launch_one<Op, NS, true>(h, n_vec, tail, cfg, cus, s)
-                           : launch_one<Op, NS, false>(h, n_vec, tail, cfg, cus, s);
+    return cfg.nontemporal ? launch_one<Op, NS, true>(h, n_vec, tail, cfg, dev, s)
+                           : launch_one<Op, NS, false>(h, n_vec, tail, cfg, dev, s);
   } else {
-    return launch_many<Op, NS, NO>(h, n_vec, tail, cfg, cus, s);
+    return launch_many<Op, NS, NO>(h, n_vec, tail, cfg, dev, s);
   }
 }
 
 template <class Op, int NS>
 hipError_t launch_ns(const void *const *src, const double *w, int n_out, void *const *out,
-                     int64_t numel, int64_t sv, const cheb_launch_config &cfg, int cus,
+                     int64_t numel, int64_t sv, const cheb_launch_config &cfg, const Gpu &cus,
                      hipStream_t s) {
   switch (n_out) {
     case 1: return launch_ns_no<Op, NS, 1>(src, w, out, numel, sv, cfg, cus, s);
@@ -350,7 +392,7 @@ hipError_t launch_ns(const void *const *src, const double *w, int n_out, void *c
 template <class Op>
 hipError_t launch_op(const void *const *src, int n, const double *w, int n_out,
                      void *const *out, int64_t numel, int64_t sv,
-                     const cheb_launch_config &cfg, int cus, hipStream_t s) {
+                     const cheb_launch_config &cfg, const Gpu &cus, hipStream_t s) {
   switch (n) {
     case 1: return launch_ns<Op, 1>(src, w, n_out, out, numel, sv, cfg, cus, s);
     case 2: return launch_ns<Op, 2>(src, w, n_out, out, numel, sv, cfg, cus, s);
@@ -586,8 +628,8 @@ hipError_t launch_residual_dec(int n, const uint64_t *base, const double *w, con
 int launch_combine(int dtype, const void *const *src, int n, const double *w, int n_out,
                    void *const *out, int64_t numel, int64_t super_vecs, hipStream_t stream) {
   if (numel == 0) return ok();
-  int cus = 0;
-  int rc = device_cus(&cus);
+  Gpu cus{0, 0, 0};
+  int rc = device_info(&cus.cus, &cus.lds_per_cu);
   if (rc != CHEB_OK) return rc;
   const cheb_launch_config cfg = launch_shape();
   hipError_t e;

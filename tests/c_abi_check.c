@@ -114,7 +114,7 @@ int main(int argc, char **argv) {
   CHECK(cheb_precompute_weights_variant(hist, 4, target, 1, CHEB_RHO_ALTERNATING, wv) == CHEB_OK);
 
   cheb_launch_config cfg;
-  CHECK(cheb_get_launch_config(&cfg) == CHEB_OK && cfg.block == 1024);
+  CHECK(cheb_get_launch_config(&cfg) == CHEB_OK && cfg.block == 64 && cfg.waves_per_cu == 0);
   printf("c abi ok\n");
   return 0;
 }

@@ -44,11 +44,12 @@ void worker(int id, const std::vector<double> &ref_w) {
     snprintf(want, sizeof want, "(%.17g)", dup);
     check(strstr(cheb_last_error(), want) != nullptr, "error message is this thread's");
     // launch shape: set and read back a whole setting
-    cheb_launch_config c = {id % 2 ? 256 : 1024, id % 2 ? 4 : 1, 1, 0};
+    cheb_launch_config c = {id % 2 ? 256 : 64, id % 2 ? 4 : 1, 1, 0, id % 2 ? 12 : 8};
     check(cheb_set_launch_config(&c) == CHEB_OK, "set launch shape");
     cheb_launch_config g;
     check(cheb_get_launch_config(&g) == CHEB_OK, "get launch shape");
-    check((g.block == 256 && g.unroll == 4) || (g.block == 1024 && g.unroll == 1),
+    check((g.block == 256 && g.unroll == 4 && g.waves_per_cu == 12) ||
+              (g.block == 64 && g.unroll == 1 && g.waves_per_cu == 8),
           "launch shape is one whole setting");
     // a table per thread
     cheb_table *t = nullptr;

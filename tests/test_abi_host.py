@@ -47,7 +47,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_version():
-    assert cheb.cheb_version() == 3
+    assert cheb.cheb_version() == 4
 
 
 def _wtol(w, factor=8.0):
@@ -380,13 +380,20 @@ def test_combine_validation_before_launch():
 
 def test_launch_config_roundtrip_and_validation():
     old = cheb.cheb_get_launch_config()
-    assert old == {"block": 1024, "unroll": 1, "nontemporal": 1, "blocks_per_cu": 0}
+    assert old == {"block": 64, "unroll": 1, "nontemporal": 1, "blocks_per_cu": 0,
+                   "waves_per_cu": 0}
+    assert old == cheb.DEFAULT_LAUNCH_CONFIG
     try:
-        cheb.cheb_set_launch_config(256, 2, 0, 8)
+        cheb.cheb_set_launch_config(256, 2, 0, 8, 12)
         assert cheb.cheb_get_launch_config() == {"block": 256, "unroll": 2, "nontemporal": 0,
-                                                 "blocks_per_cu": 8}
+                                                 "blocks_per_cu": 8, "waves_per_cu": 12}
+        for w in (-1, 1, 32):
+            cheb.cheb_set_launch_config(64, 1, 1, 0, w)
+            assert cheb.cheb_get_launch_config()["waves_per_cu"] == w
+        cheb.cheb_set_launch_config(256, 2, 0, 8, 12)
         for bad in [(256, 3, 1, 0), (256, 4, 2, 0), (256, 4, 1, -1), (256, 4, 1, 65),
-                    (128, 1, 1, 0), (512, 4, 1, 0), (1024, 2, 1, 0)]:
+                    (128, 1, 1, 0), (512, 4, 1, 0), (1024, 2, 1, 0), (64, 2, 1, 0),
+                    (64, 1, 1, 0, -2), (64, 1, 1, 0, 33)]:
             with pytest.raises(cheb.ChebError):
                 cheb.cheb_set_launch_config(*bad)
         assert cheb.cheb_get_launch_config()["block"] == 256     # unchanged by failures

@@ -3,7 +3,8 @@ they are credited with: each reading kind's output is the XOR of exactly the
 vectors it should read (contiguous streams, or the lanes of the interleaved
 layout), the write-only kind writes every vector, the window kind wraps its
 stores into the window, and the read-only kinds leave the destination
-untouched.  Small sizes with a ragged last block."""
+untouched.  Small sizes with a ragged last block, in both launch shapes
+(1024-lane blocks, and 64-lane blocks under an occupancy cap)."""
 import ctypes
 import os
 
@@ -23,14 +24,14 @@ def _lib():
     lib = ctypes.CDLL(LIB)
     lib.ceiling_stream.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_void_p), ctypes.c_int,
                                    ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
-                                   ctypes.c_void_p]
+                                   ctypes.c_int, ctypes.c_void_p]
     lib.ceiling_stream.restype = ctypes.c_int
     return lib
 
 
-def _run(lib, kind, srcs, n_src, dst, n_vec, window=0):
+def _run(lib, kind, srcs, n_src, dst, n_vec, window=0, waves=0):
     arr = (ctypes.c_void_p * max(1, len(srcs)))(*[s.data_ptr() for s in srcs]) if srcs else None
-    rc = lib.ceiling_stream(kind, arr, n_src, dst.data_ptr(), n_vec, window,
+    rc = lib.ceiling_stream(kind, arr, n_src, dst.data_ptr(), n_vec, window, waves,
                             torch.cuda.current_stream().cuda_stream)
     assert rc == 0, rc
     torch.cuda.synchronize()
@@ -46,26 +47,31 @@ def _vectors(n_vec, seed):
 N_VEC = 3 * 2048 + 517           # three whole 32 KiB chunks and a part
 
 
-def test_contiguous_kinds():
+WAVES = [0, 8, 3, 32]
+
+
+@pytest.mark.parametrize("waves", WAVES)
+def test_contiguous_kinds(waves):
     lib = _lib()
     srcs = [_vectors(N_VEC, 10 + k) for k in range(6)]
     x = srcs[0].clone()
     for s in srcs[1:]:
         x ^= s
     out = torch.zeros(N_VEC, 4, dtype=torch.int32, device="cuda")
-    _run(lib, 1, srcs, 6, out, N_VEC)                       # 6 reads, 1 write
+    _run(lib, 1, srcs, 6, out, N_VEC, waves=waves)          # 6 reads, 1 write
     assert torch.equal(out, x)
-    _run(lib, 1, srcs[:1], 1, out, N_VEC)                   # copy
+    _run(lib, 1, srcs[:1], 1, out, N_VEC, waves=waves)      # copy
     assert torch.equal(out, srcs[0])
     out.zero_()
-    _run(lib, 0, srcs, 6, out, N_VEC)                       # read only: no store
+    _run(lib, 0, srcs, 6, out, N_VEC, waves=waves)          # read only: no store
     assert not out.any()
-    _run(lib, 3, [], 1, out, N_VEC)                         # write only
+    _run(lib, 3, [], 1, out, N_VEC, waves=waves)            # write only
     idx = torch.arange(N_VEC, device="cuda", dtype=torch.int32)
     assert torch.equal(out[:, 0], idx) and not out[:, 1:].any()
 
 
-def test_interleaved_kinds():
+@pytest.mark.parametrize("waves", WAVES)
+def test_interleaved_kinds(waves):
     lib = _lib()
     n = 6
     chunks = -(-N_VEC // 2048)
@@ -75,13 +81,13 @@ def test_interleaved_kinds():
     for k in range(1, n):
         x ^= lanes[:, k].reshape(-1, 4)[:N_VEC]
     out = torch.zeros(N_VEC, 4, dtype=torch.int32, device="cuda")
-    _run(lib, 2, [region], n, out, N_VEC)
+    _run(lib, 2, [region], n, out, N_VEC, waves=waves)
     assert torch.equal(out, x)
     out.zero_()
-    _run(lib, 4, [region], n, out, N_VEC)                   # read only: no store
+    _run(lib, 4, [region], n, out, N_VEC, waves=waves)      # read only: no store
     assert not out.any()
     window = 1024
-    _run(lib, 5, [region], n, out, N_VEC, window)           # stores wrap into the window
+    _run(lib, 5, [region], n, out, N_VEC, window, waves)    # stores wrap into the window
     assert not out[window:].any()
     # several vectors land on each window slot and any of them may be the
     # last written, so check that every slot holds one that maps to it
@@ -97,7 +103,20 @@ def test_refused_arguments():
     out = torch.zeros(16, 4, dtype=torch.int32, device="cuda")
     srcs = [_vectors(16, 1)]
     arr = (ctypes.c_void_p * 1)(srcs[0].data_ptr())
-    assert lib.ceiling_stream(6, arr, 1, out.data_ptr(), 16, 0, None) == -1
-    assert lib.ceiling_stream(1, arr, 9, out.data_ptr(), 16, 0, None) == -1
-    assert lib.ceiling_stream(5, arr, 1, out.data_ptr(), 16, 3, None) == -1      # not a power of 2
-    assert lib.ceiling_stream(5, arr, 1, out.data_ptr(), 16, 32, None) == -1     # past n_vec
+    assert lib.ceiling_stream(6, arr, 1, out.data_ptr(), 16, 0, 0, None) == -1
+    assert lib.ceiling_stream(1, arr, 9, out.data_ptr(), 16, 0, 0, None) == -1
+    assert lib.ceiling_stream(5, arr, 1, out.data_ptr(), 16, 3, 0, None) == -1   # not a power of 2
+    assert lib.ceiling_stream(5, arr, 1, out.data_ptr(), 16, 32, 0, None) == -1  # past n_vec
+    assert lib.ceiling_stream(1, arr, 1, out.data_ptr(), 16, 0, 2, None) == -1   # cap too low
+    assert lib.ceiling_stream(1, arr, 1, out.data_ptr(), 16, 0, 33, None) == -1  # cap too high
+
+
+def test_lds_per_cu_reported():
+    """The occupancy cap divides the LDS the runtime reports per compute
+    unit; gfx950 has 160 KiB."""
+    lib = _lib()
+    lib.ceiling_lds_per_cu.restype = ctypes.c_int
+    lds = lib.ceiling_lds_per_cu()
+    assert lds >= 64 * 1024, lds
+    if "gfx950" in torch.cuda.get_device_properties(0).gcnArchName:
+        assert lds == 160 * 1024, lds

@@ -186,7 +186,7 @@ def test_interleaved_workload_full_size(cfg):
     equal bit for bit to the slot layout's prediction, and a sample (random
     elements, both ends of the cache and of every segment) against the
     oracle."""
-    cheb.cheb_set_launch_config(block=1024, unroll=1, nontemporal=1, blocks_per_cu=0)
+    cheb.cheb_set_launch_config(**cheb.DEFAULT_LAUNCH_CONFIG)
     say(f"interleaved workload {cfg.name} full size: {cfg.numel} x {cfg.n_hist}")
     entries = make_history(cfg, "cuda")
     il = cheb.ChebCache(cfg.n_hist, DT[cfg.dtype], cfg.seg_numel, layout="interleaved")

@@ -28,6 +28,12 @@ SHAPES = [
     {"block": 512, "unroll": 1, "nontemporal": 1, "blocks_per_cu": 0},
     {"block": 256, "unroll": 4, "nontemporal": 0, "blocks_per_cu": 2},
     {"block": 1024, "unroll": 1, "nontemporal": 1, "blocks_per_cu": 8},
+    {"block": 64, "unroll": 1, "nontemporal": 1, "blocks_per_cu": 0, "waves_per_cu": 0},
+    {"block": 64, "unroll": 1, "nontemporal": 0, "blocks_per_cu": 0, "waves_per_cu": 4},
+    {"block": 64, "unroll": 1, "nontemporal": 1, "blocks_per_cu": 4, "waves_per_cu": -1},
+    {"block": 64, "unroll": 1, "nontemporal": 1, "blocks_per_cu": 0, "waves_per_cu": 32},
+    {"block": 256, "unroll": 1, "nontemporal": 1, "blocks_per_cu": 0, "waves_per_cu": 12},
+    {"block": 1024, "unroll": 1, "nontemporal": 1, "blocks_per_cu": 0, "waves_per_cu": 8},
 ]
 
 
@@ -69,7 +75,8 @@ def test_combine_all_sizes(dtype, n):
                      f"n={n} numel={numel}")
 
 
-@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "b{block}_u{unroll}_nt{nontemporal}_g{blocks_per_cu}".format(**s))
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "b{block}_u{unroll}_nt{nontemporal}_g{blocks_per_cu}_w{waves}".format(
+                             waves=s.get("waves_per_cu", 0), **s))
 @pytest.mark.parametrize("dtype", ["bf16", "f16", "f32"])
 def test_combine_launch_shapes(shape, dtype):
     cheb.cheb_set_launch_config(**shape)
@@ -315,7 +322,7 @@ def test_workload_full_size_sampled(cfg):
     """Full cache shape, default launch shape (the one the benchmark times):
     the oracle recomputes a sample of outputs (random elements, both ends of
     the cache and of every segment) from the same stored inputs."""
-    cheb.cheb_set_launch_config(block=1024, unroll=1, nontemporal=1, blocks_per_cu=0)
+    cheb.cheb_set_launch_config(**cheb.DEFAULT_LAUNCH_CONFIG)
     say(f"workload {cfg.name} full size: {cfg.numel} elements x {cfg.n_hist}")
     cache, entries, outs, ws = _run_workload(cfg, cfg.nodes, cfg.targets)
     idx = _sample_indices(cfg.numel, cache.seg_offset, cache.seg_numel, 1 << 20, cfg.seed)

@@ -70,9 +70,9 @@ def test_weights_and_tables_built_concurrently_match():
 def test_launch_shape_updates_are_whole():
     """Concurrent set/get of the launch shape never returns a mix of two
     settings."""
-    shapes = [dict(block=256, unroll=4, nontemporal=1, blocks_per_cu=0),
-              dict(block=512, unroll=2, nontemporal=0, blocks_per_cu=2),
-              dict(block=1024, unroll=1, nontemporal=1, blocks_per_cu=0)]
+    shapes = [dict(block=256, unroll=4, nontemporal=1, blocks_per_cu=0, waves_per_cu=12),
+              dict(block=512, unroll=2, nontemporal=0, blocks_per_cu=2, waves_per_cu=-1),
+              dict(block=64, unroll=1, nontemporal=1, blocks_per_cu=0, waves_per_cu=0)]
     old = cheb.cheb_get_launch_config()
 
     def worker(i):
