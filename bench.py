@@ -505,7 +505,7 @@ def device_summary(torch):
     return {"name": p.name, "gcn_arch": getattr(p, "gcnArchName", None),
             "compute_units": p.multi_processor_count,
             "lds_per_cu_bytes": lds if lds >= 0 else None,
-            "lds_reserved_per_64_lane_block_at_8_waves": lds // 8 // 1024 * 1024
+            "lds_reserved_per_64_lane_block_at_7_waves": lds // 7 // 512 * 512
             if lds > 0 else None}
 
 
@@ -522,7 +522,8 @@ def stream_ceilings(torch, slots_cache, il_cache, out, reps=10, warmup=2):
     rate the reads allow when the stores cost less.  Every case runs in both
     launch shapes of the prediction: 1024-lane blocks at full occupancy, and
     64-lane blocks capped at 8 waves per compute unit (suffix _w8); the
-    6:1 streams also at 12 waves (_w12)."""
+    6:1 streams also at 7 waves (_w7), the cap the prediction takes for six
+    entries and one output."""
     import ctypes
     lib = ctypes.CDLL(CEILING_LIB)
     lib.ceiling_stream.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_void_p), ctypes.c_int,
@@ -552,9 +553,9 @@ def stream_ceilings(torch, slots_cache, il_cache, out, reps=10, warmup=2):
     shaped = []
     for name, kind, src, nbytes, window in cases:
         shaped.append((name, kind, src, nbytes, window, 0))
-        shaped.append((name + "_w8", kind, src, nbytes, window, 8))
         if name.startswith("mix_6_1") and window == 0:
-            shaped.append((name + "_w12", kind, src, nbytes, window, 12))
+            shaped.append((name + "_w7", kind, src, nbytes, window, 7))
+        shaped.append((name + "_w8", kind, src, nbytes, window, 8))
     res = {}
     for name, kind, src, nbytes, window, waves in shaped:
         arr = (ctypes.c_void_p * max(1, len(src)))(*src) if src else None

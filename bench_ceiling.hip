@@ -111,8 +111,8 @@ hipError_t launch(int kind, int n_src, const Srcs &s, u32x4 *d, uint32_t n, uint
 //   window_vecs  kind 5 only: a power of two, 1 .. n_vec.
 //   waves_per_cu  0: 1024-lane blocks at full occupancy; 3..32: 64-lane
 //          blocks, each reserving 1/waves_per_cu of the compute unit's LDS
-//          (at most 64 KiB), so that at most that many waves share a
-//          compute unit.
+//          (rounded down to 512 bytes, at most 64 KiB), so that about that
+//          many waves share a compute unit.
 // Returns 0, or -1 for arguments out of range, or the HIP error code of the
 // launch or of the device query.
 extern "C" __attribute__((visibility("default"))) int ceiling_stream(int kind, const void *const *src,
@@ -146,7 +146,7 @@ extern "C" __attribute__((visibility("default"))) int ceiling_stream(int kind, c
     if (e == hipSuccess)
       e = hipDeviceGetAttribute(&lds_per_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev);
     if (e != hipSuccess) return int(e);
-    const size_t lds = size_t(lds_per_cu / waves_per_cu) / 1024 * 1024;
+    const size_t lds = size_t(lds_per_cu / waves_per_cu) / 512 * 512;
     if (lds > (size_t(64) << 10)) return -1;
     e = launch<64>(kind, n_src, s, d, n, mask, lds, st);
   }

@@ -531,17 +531,19 @@ CHEB_API int cheb_residual_reduce(const void *const *seg_src, const int64_t *seg
  *                covers the whole problem); 1..64: a persistent grid of that
  *                many blocks per compute unit, each looping over tiles.
  *   waves_per_cu  cap on the prediction kernel's 64-lane waves resident on
- *                one compute unit.  0: chosen from the history size (8 for 5
- *                or more entries, 12 for 4, 16 for 3, 24 for 2, none for 1);
- *                -1: no cap; 1..32: that cap.  Each block reserves an equal
- *                share of the compute unit's LDS, which the kernel never
+ *                one compute unit.  0: chosen from the history size n and
+ *                the number of outputs: for one output max(6, 44/n rounded)
+ *                (7 for 6 entries, 9 for 5), for several max(6, 36/n
+ *                rounded), no cap for n <= 2; -1: no cap; 1..32: that cap.
+ *                Each block reserves an equal share of the compute unit's
+ *                LDS, rounded down to 512 bytes, which the kernel never
  *                touches, so that no more blocks fit; the cap applies only
  *                where that share is at most 64 KiB (64- and 256-thread
  *                blocks) and is ignored otherwise.
  * Default {64, 1, 1, 0, 0}.  On MI355X a bf16 history of 5-6 entries
- * streams at about 0.86 of the HBM peak with 8 waves per compute unit,
- * against 0.77 with 1024-thread blocks at full occupancy: fewer waves keep
- * enough loads in flight without crowding out the output's stores.  With
+ * streams at about 0.85 of the HBM peak under the chosen cap, against 0.75
+ * with 1024-thread blocks at full occupancy: fewer waves keep enough loads
+ * in flight without crowding out the output's stores.  With
  * block 1024, a problem under 4096 vectors per compute unit runs with
  * 256-thread blocks.  The history ring's push (a copy) always runs at full
  * occupancy.  Errors: CHEB_E_INVAL. */

@@ -275,22 +275,24 @@ struct Gpu {
   int waves;       // occupancy cap in waves per compute unit, 0: none
 };
 
-// Waves per compute unit the prediction streams best with, by history size.
-// Measured on MI355X (FLUX-sized streams): the mix of NS reads and the
-// output's writes runs fastest with about 48 KiB of loads in flight per
-// compute unit (8 waves of 64 lanes x NS x 16 bytes for NS = 5, 6); more
-// waves flood the memory queues and slow the writes, fewer leave latency
-// uncovered.
-int auto_waves(int ns) {
-  if (ns >= 5) return 8;
-  if (ns == 4) return 12;
-  if (ns == 3) return 16;
-  if (ns == 2) return 24;
-  return 0;
+// Waves per compute unit the prediction streams best with, from the history
+// size NS and the number of outputs NO.  Measured on MI355X (FLUX- and
+// DiT-sized bf16 streams): the mix of NS reads and the output's writes runs
+// fastest with about 44 KiB of loads in flight per compute unit for one
+// output (NS x 1 KiB per 64-lane wave: 7 waves for NS = 6, 9 for NS = 5)
+// and about 36 KiB for several (6 and 7); more waves flood the memory queues
+// and slow the writes.  Below 6 waves the latency is no longer covered and
+// the rate falls steeply, hence the floor.  Two entries or fewer stream as
+// well at full occupancy: no cap.
+int auto_waves(int ns, int no) {
+  if (ns <= 2) return 0;
+  const int kib = no == 1 ? 44 : 36;
+  return std::max(6, (kib + ns / 2) / ns);
 }
 
-// Dynamic LDS a block reserves, and never touches, so that at most `waves`
-// waves of the kernel share a compute unit (the LDS is what runs out).  Zero
+// Dynamic LDS a block reserves, and never touches, so that about `waves`
+// waves of the kernel share a compute unit (the LDS is what runs out): an
+// equal share of the compute unit's LDS, rounded down to 512 bytes.  Zero
 // when there is no cap, when the cap is at the hardware's own limit, or when
 // one block would need more than the default 64 KiB of dynamic LDS.
 template <int BLK>
@@ -299,7 +301,7 @@ size_t occupancy_lds(const Gpu &g) {
   if (g.waves <= 0 || g.lds_per_cu <= 0) return 0;
   const int blocks = std::max(1, g.waves / kWavesPerBlock);
   if (blocks * kWavesPerBlock >= 32) return 0;
-  const size_t per = size_t(g.lds_per_cu / blocks) / 1024 * 1024;
+  const size_t per = size_t(g.lds_per_cu / blocks) / 512 * 512;
   return per <= size_t(64) << 10 ? per : 0;
 }
 
@@ -355,7 +357,7 @@ hipError_t launch_ns_no(const void *const *src, const double *w, void *const *ou
                         const Gpu &dev0, hipStream_t s) {
   constexpr int kVec = 16 / int(sizeof(typename Op::E));
   Gpu dev = dev0;
-  dev.waves = cfg.waves_per_cu == 0 ? auto_waves(NS) : std::max(0, cfg.waves_per_cu);
+  dev.waves = cfg.waves_per_cu == 0 ? auto_waves(NS, NO) : std::max(0, cfg.waves_per_cu);
   Hist<NS, NO, typename Op::W> h;
   h.super = uint64_t(super_vecs);
   for (int k = 0; k < NS; ++k) h.p[k] = static_cast<const u32x4 *>(src[k]);
