@@ -539,7 +539,9 @@ CHEB_API int cheb_residual_reduce(const void *const *seg_src, const int64_t *seg
  *                LDS, rounded down to 512 bytes, which the kernel never
  *                touches, so that no more blocks fit; the cap applies only
  *                where that share is at most 64 KiB (64- and 256-thread
- *                blocks) and is ignored otherwise.
+ *                blocks) and is ignored otherwise.  While a prediction
+ *                runs, kernels on other streams find that LDS taken; -1
+ *                leaves it free.
  * Default {64, 1, 1, 0, 0}.  On MI355X a bf16 history of 5-6 entries
  * streams at about 0.85 of the HBM peak under the chosen cap, against 0.75
  * with 1024-thread blocks at full occupancy: fewer waves keep enough loads
