@@ -338,6 +338,38 @@ def test_workload_full_size_sampled(cfg):
     torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("cfg", [c for c in CONFIGS if c.name != "tiny"], ids=lambda c: c.name)
+def test_workload_full_size_every_element(cfg):
+    """Full cache shape, interleaved history and the default launch shape
+    (what the benchmark times), the workload's farthest target: every
+    element against the oracle, in chunks of 2^26 elements, with the
+    history read back from the ring."""
+    cheb.cheb_set_launch_config(**cheb.DEFAULT_LAUNCH_CONFIG)
+    say(f"workload {cfg.name} full size, every element: {cfg.numel} x {cfg.n_hist}")
+    entries = make_history(cfg, "cuda")
+    cache = cheb.ChebCache(cfg.n_hist, DT[cfg.dtype], cfg.seg_numel, layout="interleaved")
+    for x, e in zip(cfg.nodes, entries):
+        cache.push(x, split_segments(e, cfg))
+    del entries
+    t = cfg.targets[-1]
+    out, _ = cache.extrapolate_at(t)
+    stored = [cache.entry(k)[:cfg.numel] for k in range(cfg.n_hist)]
+    torch.cuda.synchronize()
+    w_or = oracle.weights_row(cfg.nodes, t)
+    chunk = 1 << 26
+    worst = 0.0
+    for start in range(0, cfg.numel, chunk):
+        stop = min(cfg.numel, start + chunk)
+        hosts = [to_host_bits(h[start:stop]) for h in stored]
+        e, _ = check_parity(to_host_bits(out[start:stop]), hosts, w_or, cfg.dtype,
+                            f"{cfg.name} t={t} elements {start}..{stop}")
+        worst = max(worst, e)
+    say(f"  t={t}: floored error {worst:.3e} over all {cfg.numel} elements")
+    cache.close()
+    del stored, out, cache
+    torch.cuda.empty_cache()
+
+
 def test_tiny_recovers_quadratic():
     """Tiny workload: F_k = A + B tau + C tau^2 + 1e-3 noise, stored in fp32.
     The prediction at the next timesteps equals the quadratic at the target
