@@ -410,7 +410,10 @@ hipError_t launch_op(const void *const *src, int n, const double *w, int n_out,
 // ---- full-step push: segment gather into one slot --------------------------
 
 constexpr int kGatherMax = 64;
-constexpr int kGatherBlock = 1024;  // one 16-byte vector per lane
+// One 16-byte vector per lane.  256-lane blocks copy into an interleaved
+// lane 4-5% faster than 1024-lane ones on MI355X (and as fast into a
+// contiguous slot); 64-lane blocks lose on the blocks that find no work.
+constexpr int kGatherBlock = 256;
 constexpr uint32_t kGatherChunk = kGatherBlock;  // vectors per block
 
 struct GatherArgs {
@@ -420,7 +423,7 @@ struct GatherArgs {
   int32_t n;
 };
 
-// Grid: x = 1024-vector chunk within a segment, y = segment.  Blocks past
+// Grid: x = 256-vector chunk within a segment, y = segment.  Blocks past
 // their segment's end return at once, so no block searches for its
 // segment.  Source reads and slot writes are streaming (each byte is touched
 // once per push), so both carry the non-temporal hint.  Vector v of the
