@@ -91,6 +91,34 @@ def test_combine_launch_shapes(shape, dtype):
         check_parity(to_host_bits(out), [to_host_bits(s) for s in srcs], w, dtype, str(shape))
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f16", "f32"])
+def test_launch_shapes_give_identical_bits(dtype):
+    """Each element's sum runs in the same order whatever the launch shape,
+    so every shape and occupancy cap of the tuning interface gives the same
+    bits, for one output and for several (ragged size, interleaved-layout
+    chunk formula not involved)."""
+    n, numel = 6, 3 * 65536 + 4099
+    srcs = _rand(n, numel, dtype, seed=77)
+    w = oracle.weights([2, 5, 10, 14, 20, 25], [26, 27, 28])
+    ref_one, ref_many = None, None
+    for shape in SHAPES + [{"block": 64, "unroll": 1, "nontemporal": 1, "blocks_per_cu": 0,
+                            "waves_per_cu": wv} for wv in (-1, 1, 6, 9, 16, 24)]:
+        cheb.cheb_set_launch_config(**shape)
+        one = torch.empty(numel, dtype=DT[dtype], device="cuda")
+        cheb.combine(srcs, w[0], one)
+        many = [torch.empty(numel, dtype=DT[dtype], device="cuda") for _ in range(3)]
+        cheb.combine_multi(srcs, w, many)
+        torch.cuda.synchronize()
+        if ref_one is None:
+            ref_one, ref_many = one, many
+            check_parity(to_host_bits(one), [to_host_bits(s) for s in srcs], w[0], dtype, str(shape))
+            continue
+        assert torch.equal(one.view(torch.uint8), ref_one.view(torch.uint8)), shape
+        for a, b in zip(many, ref_many):
+            assert torch.equal(a.view(torch.uint8), b.view(torch.uint8)), shape
+        assert torch.equal(many[0].view(torch.uint8), one.view(torch.uint8)), shape
+
+
 def test_combine_empty_and_nonzero_stream():
     out = torch.empty(0, dtype=torch.bfloat16, device="cuda")
     cheb.combine([out, out], [0.5, 0.5], out)
